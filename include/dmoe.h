@@ -1,0 +1,171 @@
+/*
+ * dmoe.h -- C ABI of libdmoe.so: one Decentralized Mixture-of-Experts layer
+ * (Ryabinin & Gusev, arXiv 2002.04013), forward and backward, on one gfx950 GPU.
+ *
+ * The layer (Sec. 3.1, Sec. 3.2, Eq. 1):
+ *   experts sit on a d-dimensional grid, expert f has uid (u_0 .. u_{d-1}), u_i in [0, M);
+ *   the gate is d linear layers g_i : R^D -> R^M and scores expert f by
+ *       g(x, f) = sum_i g_i(x)[u_i];
+ *   TopK(x) are the k experts with the highest g (ties: lower flat index);
+ *   DMoE(x) = sum_{f in TopK(x)} f(x) exp(g(x,f)) / sum_{f' in TopK(x)} exp(g(x,f')),
+ *   with experts that do not respond excluded and the remaining weights
+ *   renormalised to sum to 1 (Sec. 3.2).
+ * Each expert is the feed-forward block f(x) = W2 act(W1 x + b1) + b2 (Sec. 4.1).
+ *
+ * Conventions shared by every entry point
+ *   - Every array pointer is a DEVICE pointer, row-major, owned by the caller.
+ *     The library allocates nothing, frees nothing and never synchronises; all
+ *     work is enqueued on `stream` (a hipStream_t passed as void*; NULL = the
+ *     default stream).  Results are ready when the stream reaches them.
+ *   - Flat expert index: flat = sum_i u_i * M^(d-1-i) (u_0 most significant).
+ *     N = M^d experts; gate column c = i*M + u belongs to grid dimension i.
+ *   - dtype DMOE_BF16: x, gate and expert weights/biases, activations, outputs
+ *     and their gradients are bf16 (uint16 bit patterns); all arithmetic
+ *     accumulates in fp32 (gate scores in fp64).  DMOE_F32: all of those are fp32.
+ *     w, dw, dg, g and scores are always fp32; indices are int32; alive is uint8.
+ *   - "pairs": pair p = t*k + j is token t's j-th chosen expert.  P_max = T*k.
+ *   - Buffers are sized for P_max rows; the number of rows actually used,
+ *     offsets[N], stays on the device (no host synchronisation on the path).
+ *   - Results are bitwise reproducible from run to run (no floating-point atomics).
+ *   - Supported: 1 <= d <= 4, 1 <= M, d*M <= 128, 1 <= k <= min(N, 8),
+ *     N <= 16384, T >= 0, D and H multiples of 64, pointers 16-byte aligned.
+ *
+ * Return codes: DMOE_OK (0); DMOE_EINVAL (-1) null required pointer or bad
+ * dims; DMOE_EUNSUPPORTED (-2) shape/alignment outside the supported set;
+ * DMOE_EHIP (-3) a launch failed (hipGetLastError).  Device faults surface at
+ * the caller's next synchronisation, as HIP reports them.
+ */
+#ifndef DMOE_H
+#define DMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { DMOE_OK = 0, DMOE_EINVAL = -1, DMOE_EUNSUPPORTED = -2, DMOE_EHIP = -3 };
+enum { DMOE_F32 = 0, DMOE_BF16 = 1 };          /* dmoe_dims.dtype */
+enum { DMOE_RELU = 0, DMOE_GELU = 1 };         /* dmoe_dims.act; GELU is the erf form */
+
+typedef struct {
+  int64_t T;      /* tokens */
+  int64_t D;      /* d_model */
+  int64_t H;      /* expert hidden size */
+  int32_t d;      /* grid dimensions */
+  int32_t M;      /* indices per grid dimension */
+  int32_t k;      /* experts chosen per token */
+  int32_t dtype;  /* DMOE_F32 or DMOE_BF16 */
+  int32_t act;    /* DMOE_RELU or DMOE_GELU */
+  int32_t reserved;
+} dmoe_dims;
+
+/* Bytes of device workspace every entry point below needs for these dims
+ * (one buffer of this size serves all of them; it may be reused between calls
+ * on the same stream).  Returns 0 for invalid dims. */
+size_t dmoe_workspace_bytes(const dmoe_dims* dims);
+
+/* Static text for a return code. */
+const char* dmoe_strerror(int code);
+
+/* Gate scores, exact TopK over the grid and Eq. 1 weights (Sec. 3.2; Eq. 1; App. C).
+ *   x      [T, D]      layer input
+ *   Wg     [d*M, D]    rows i*M .. i*M+M-1 are the weight of g_i (nn.Linear layout)
+ *   bg     [d*M]       gate bias, or NULL for none
+ *   alive  [N] uint8   1 = the expert responds; NULL = all respond
+ * outputs
+ *   idx    [T, k] int32  chosen flat expert ids, best first: by g descending,
+ *                        ties to the lower flat index
+ *   w      [T, k] fp32   Eq. 1 weights over the chosen experts that are alive,
+ *                        renormalised to sum to 1; 0 for dead ones; all 0 if
+ *                        every chosen expert is dead
+ *   g      [T, k] fp32   chosen totals g(x, f), or NULL
+ *   scores [T, d*M] fp32 per-dimension decision scores g_i(x), or NULL
+ * Selection compares the fp32 rounding of each g_i(x)[u] (computed with fp64
+ * accumulation) and adds the d fp32 values of a cell in fp64 in dim order.
+ * Uses workspace: no. */
+int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* Wg, const void* bg,
+                   const uint8_t* alive, int32_t* idx, float* w, float* g, float* scores,
+                   void* ws, void* stream);
+
+/* Group the alive pairs by expert: the per-expert batches a Runtime forms from
+ * incoming requests (Sec. 3.3), and the input each chosen expert receives (Sec. 3.2).
+ * Rows of one expert are contiguous and in token order.
+ *   x [T, D], idx [T, k], alive [N] or NULL
+ * outputs
+ *   counts    [N]       alive pairs per expert
+ *   offsets   [N+1]     exclusive prefix sum of counts (offsets[N] = rows used)
+ *   row_token [P_max]   token of each row (entries >= offsets[N] untouched)
+ *   pos       [T, k]    row of each pair, -1 if its expert is dead
+ *   x_perm    [P_max, D] x_perm[r] = x[row_token[r]] (rows >= offsets[N] untouched)
+ * Uses workspace. */
+int dmoe_dispatch(const dmoe_dims* dims, const void* x, const int32_t* idx,
+                  const uint8_t* alive, int32_t* counts, int32_t* offsets, int32_t* row_token,
+                  int32_t* pos, void* x_perm, void* ws, void* stream);
+
+/* Expert feed-forward blocks on the grouped rows (the Runtime Forward, Sec. 3.3):
+ * for rows r of expert e,  h = x_perm W1_e^T + b1_e,  a = act(h),  y = a W2_e^T + b2_e.
+ *   offsets [N+1] (from dmoe_dispatch), x_perm [P_max, D]
+ *   W1 [N, H, D], b1 [N, H], W2 [N, D, H], b2 [N, D]
+ * outputs (rows < offsets[N] written)
+ *   h [P_max, H] pre-activation, a [P_max, H] activation, y_perm [P_max, D]
+ * Uses workspace. */
+int dmoe_expert_ffn_fwd(const dmoe_dims* dims, const int32_t* offsets, const void* x_perm,
+                        const void* W1, const void* b1, const void* W2, const void* b2,
+                        void* h, void* a, void* y_perm, void* ws, void* stream);
+
+/* Weighted average of Eq. 1:  y[t] = sum_j w[t,j] y_perm[pos[t,j]] over pairs with
+ * pos >= 0, in slot order, fp32 accumulation.  y [T, D] written (zeros for tokens
+ * with no alive expert).  Uses workspace: no. */
+int dmoe_combine(const dmoe_dims* dims, const void* y_perm, const int32_t* pos,
+                 const float* w, void* y, void* stream);
+
+/* Backward of the weighted average (derivative of Eq. 1 in w and in f(x)):
+ *   dy_perm[pos[t,j]] = w[t,j] dy[t]          (rows of alive pairs)
+ *   dw[t,j] = <dy[t], y_perm[pos[t,j]]>        (0 for dead pairs), fp32
+ * Uses workspace: no. */
+int dmoe_combine_bwd(const dmoe_dims* dims, const void* dy, const void* y_perm,
+                     const int32_t* pos, const float* w, void* dy_perm, float* dw,
+                     void* stream);
+
+/* Backward of the Eq. 1 weights and of the gate layers (Sec. 3.2).  TopK is
+ * piecewise constant; the gradient reaches the gate through the softmax over
+ * the chosen alive experts only:
+ *   dg[t,j] = w[t,j] (dw[t,j] - sum_l w[t,l] dw[t,l])   (0 for dead pairs)
+ *   ds[t, i*M + u_i(idx[t,j])] += dg[t,j]  for every dimension i
+ *   dWg = ds^T x   [d*M, D]  (dtype of Wg),   dbg = sum_t ds  [d*M] (dtype of Wg)
+ * The gate's share of dx (ds Wg) is added by dmoe_dispatch_bwd.
+ *   x [T, D], idx [T, k], w [T, k], dw [T, k], alive [N] or NULL
+ * outputs: dg [T, k] fp32, dWg, dbg (dbg may be NULL).  Uses workspace. */
+int dmoe_gate_topk_bwd(const dmoe_dims* dims, const void* x, const int32_t* idx,
+                       const float* w, const float* dw, const uint8_t* alive, float* dg,
+                       void* dWg, void* dbg, void* ws, void* stream);
+
+/* Backward of the expert blocks (the Runtime Backward, Sec. 3.3, which returns
+ * input gradients; the parameter update is left to the caller):
+ *   dh = (dy_perm W2_e) * act'(h)       [P_max, H]  (may alias h: h is then overwritten)
+ *   dx_perm = dh W1_e                   [P_max, D]
+ *   dW2_e = dy_perm_e^T a_e,  db2_e = sum of dy_perm_e rows
+ *   dW1_e = dh_e^T x_perm_e,  db1_e = sum of dh_e rows
+ * dW1 [N,H,D], db1 [N,H], dW2 [N,D,H], db2 [N,D]: written only for experts with
+ * counts[e] > 0 (an expert with no rows has zero gradient; its slots are not touched).
+ * Uses workspace. */
+int dmoe_expert_ffn_bwd(const dmoe_dims* dims, const int32_t* offsets, const int32_t* counts,
+                        const void* x_perm, const void* h, const void* a, const void* dy_perm,
+                        const void* W1, const void* W2, void* dh, void* dx_perm, void* dW1,
+                        void* db1, void* dW2, void* db2, void* ws, void* stream);
+
+/* Input gradient of the layer: the experts' input gradients summed over each
+ * token's alive pairs (slot order), plus, when idx, dg and Wg are all non-NULL,
+ * the gate's share sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])].  fp32 accumulation,
+ * one rounding.  dx [T, D] written.  Uses workspace: no. */
+int dmoe_dispatch_bwd(const dmoe_dims* dims, const void* dx_perm, const int32_t* pos,
+                      const int32_t* idx, const float* dg, const void* Wg, void* dx,
+                      void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DMOE_H */

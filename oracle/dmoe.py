@@ -29,6 +29,19 @@ def to64(a):
     return np.asarray(a, dtype=np.float64)
 
 
+def round_bf16(a):
+    """Round to the nearest value with 8 significant bits (bf16), ties to even.
+    This is the storage rounding of a layer whose activations are kept in bf16
+    (normal range; bf16 shares fp32's exponent range)."""
+    a = np.asarray(a, np.float64)
+    m, e = np.frexp(a)                      # a = m 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)
+
+
+def _identity(a):
+    return a
+
+
 # ---------------------------------------------------------------- gating (Sec. 3.2)
 
 def gate_scores(x, Wg, bg=None):
@@ -206,11 +219,14 @@ def expert_forward(X, W1, b1, W2, b2, kind):
     return h, a, y
 
 
-def expert_backward(X, h, a, dY, W1, W2, kind):
-    """Gradients of the expert block for a batch: (dX, dW1, db1, dW2, db2)."""
+def expert_backward(X, h, a, dY, W1, W2, kind, store=None):
+    """Gradients of the expert block for a batch: (dX, dW1, db1, dW2, db2).
+    store (optional) rounds the tensors a layer keeps in its storage dtype:
+    here the pre-activation gradient dH and the input gradient dX."""
+    store = store or _identity
     dA = dY @ W2
-    dH = dA * act_grad(h, kind)
-    return dH @ W1, dH.T @ X, dH.sum(axis=0), dY.T @ a, dY.sum(axis=0)
+    dH = store(dA * act_grad(h, kind))
+    return store(dH @ W1), dH.T @ X, dH.sum(axis=0), dY.T @ a, dY.sum(axis=0)
 
 
 # ------------------------------------------------------------ dispatch (Sec. 3.3)
@@ -266,13 +282,16 @@ def _expert_getter(experts):
     return lambda e: (W1[e], b1[e], W2[e], b2[e])
 
 
-def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None):
+def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, store=None):
     """DMoE(x) of Eq. 1: sum over the alive chosen experts of f(x) times its
     renormalised weight.  experts is (W1, b1, W2, b2) stacked over experts or a
     callable e -> (W1_e, b1_e, W2_e, b2_e), all fp64.  only_experts restricts the
     expert evaluation to a subset (rows of other experts stay NaN, and so does y
     for tokens that use them).  Returns a dict with the routing, the dispatch,
-    the per-row h, a, y_perm (expert-grouped order) and the layer output y."""
+    the per-row h, a, y_perm (expert-grouped order) and the layer output y.
+    store (optional) rounds the tensors a bf16 layer keeps in bf16 (h, a and the
+    expert outputs); all arithmetic stays exact."""
+    store = store or _identity
     x = np.asarray(x, np.float64)
     T, D = x.shape
     N = M ** d
@@ -288,7 +307,10 @@ def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None):
     for e in todo:
         lo, hi = offsets[e], offsets[e + 1]
         W1, b1, W2, b2 = get(e)
-        he, ae, ye = expert_forward(x[row_token[lo:hi]], W1, b1, W2, b2, kind)
+        he = x[row_token[lo:hi]] @ W1.T + b1[None, :]
+        ae = store(act(he, kind))
+        he = store(he)
+        ye = store(ae @ W2.T + b2[None, :])
         hs[e], as_[e] = he, ae
         y_perm[lo:hi] = ye
     if hs:
@@ -328,13 +350,15 @@ def gate_backward(w, dw, idx, alive, x, Wg, d, M):
     return dg, ds, ds @ np.asarray(Wg, np.float64), ds.T @ x, ds.sum(axis=0)
 
 
-def layer_backward(fwd, dy, x, Wg, experts, alive, d, M, k, kind, only_experts=None):
+def layer_backward(fwd, dy, x, Wg, experts, alive, d, M, k, kind, only_experts=None, store=None):
     """Gradients of <DMoE(x), dy> with respect to x, the gate and the experts.
 
     dw_tj = <dy_t, f_j(x_t)> for alive chosen experts; the expert f_j receives
     w_tj dy_t as its output gradient; dx gathers every expert's input gradient
     plus the gate's.  Expert gradients are returned only for experts that got
-    rows (an expert with no rows has zero gradient)."""
+    rows (an expert with no rows has zero gradient).  store (optional) rounds the
+    tensors a bf16 layer keeps in bf16 (output gradients per row, dH, dX per row)."""
+    store = store or _identity
     x = np.asarray(x, np.float64)
     dy = np.asarray(dy, np.float64)
     T, D = x.shape
@@ -347,7 +371,7 @@ def layer_backward(fwd, dy, x, Wg, experts, alive, d, M, k, kind, only_experts=N
         p = pos[:, j]
         ok = p >= 0
         dw[ok, j] = np.einsum("td,td->t", dy[ok], y_perm[p[ok]])
-        dy_perm[p[ok]] = w[ok, j][:, None] * dy[ok]
+        dy_perm[p[ok]] = store(w[ok, j][:, None] * dy[ok])
     dg, ds, dx_gate, dWg, dbg = gate_backward(w, dw, idx, alive, x, Wg, d, M)
     get = _expert_getter(experts)
     dx_perm = np.full((y_perm.shape[0], D), np.nan)
@@ -358,7 +382,8 @@ def layer_backward(fwd, dy, x, Wg, experts, alive, d, M, k, kind, only_experts=N
         lo, hi = offsets[e], offsets[e + 1]
         W1, b1, W2, b2 = get(e)
         dX, dW1, db1, dW2, db2 = expert_backward(
-            x[row_token[lo:hi]], fwd["h"][lo:hi], fwd["a"][lo:hi], dy_perm[lo:hi], W1, W2, kind)
+            x[row_token[lo:hi]], fwd["h"][lo:hi], fwd["a"][lo:hi], dy_perm[lo:hi], W1, W2, kind,
+            store)
         dx_perm[lo:hi] = dX
         grads[e] = (dW1, db1, dW2, db2)
     dx = dx_gate.copy()

@@ -1,0 +1,151 @@
+"""ctypes binding of libdmoe.so: the C ABI of include/dmoe.h, same names.
+
+Argument marshalling only: torch tensors (device memory) are passed as raw
+pointers together with the current HIP stream; every step runs in the HIP
+kernels of the library.  There is no fallback: without the built library or a
+GPU every call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdmoe.so")
+
+DMOE_F32, DMOE_BF16 = 0, 1
+DMOE_RELU, DMOE_GELU = 0, 1
+
+# every extern "C" symbol the header declares
+EXPORTS = (
+    "dmoe_workspace_bytes", "dmoe_strerror", "dmoe_gate_topk", "dmoe_dispatch",
+    "dmoe_expert_ffn_fwd", "dmoe_combine", "dmoe_combine_bwd", "dmoe_gate_topk_bwd",
+    "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd",
+)
+
+
+class DmoeError(RuntimeError):
+    pass
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int64), ("D", ctypes.c_int64), ("H", ctypes.c_int64),
+                ("d", ctypes.c_int32), ("M", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+def make_dims(T, D, H, d, M, k, dtype="bf16", act="gelu"):
+    return Dims(int(T), int(D), int(H), int(d), int(M), int(k),
+                DMOE_BF16 if dtype == "bf16" else DMOE_F32,
+                DMOE_GELU if act == "gelu" else DMOE_RELU, 0)
+
+
+_lib = None
+_P = ctypes.c_void_p
+
+
+def load(path=LIB_PATH):
+    """Load libdmoe.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise DmoeError(f"{path} is missing: build it with `python -m paper_2002_04013_amd.build`")
+    lib = ctypes.CDLL(path)
+    pd = ctypes.POINTER(Dims)
+    sig = {
+        "dmoe_workspace_bytes": (ctypes.c_size_t, [pd]),
+        "dmoe_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        "dmoe_gate_topk": (ctypes.c_int, [pd] + [_P] * 10),
+        "dmoe_dispatch": (ctypes.c_int, [pd] + [_P] * 10),
+        "dmoe_expert_ffn_fwd": (ctypes.c_int, [pd] + [_P] * 11),
+        "dmoe_combine": (ctypes.c_int, [pd] + [_P] * 5),
+        "dmoe_combine_bwd": (ctypes.c_int, [pd] + [_P] * 7),
+        "dmoe_gate_topk_bwd": (ctypes.c_int, [pd] + [_P] * 10),
+        "dmoe_expert_ffn_bwd": (ctypes.c_int, [pd] + [_P] * 16),
+        "dmoe_dispatch_bwd": (ctypes.c_int, [pd] + [_P] * 7),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch.Tensor or None")
+    if not t.is_cuda:
+        raise DmoeError("libdmoe takes device tensors only")
+    if not t.is_contiguous():
+        raise DmoeError("libdmoe takes contiguous tensors only")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(rc, name):
+    if rc != 0:
+        msg = load().dmoe_strerror(rc).decode()
+        raise DmoeError(f"{name} failed: {msg} ({rc})")
+
+
+def workspace_bytes(dims):
+    return int(load().dmoe_workspace_bytes(ctypes.byref(dims)))
+
+
+def strerror(code):
+    return load().dmoe_strerror(int(code)).decode()
+
+
+def dmoe_gate_topk(dims, x, Wg, bg, alive, idx, w, g=None, scores=None, ws=None, stream=None):
+    _check(load().dmoe_gate_topk(ctypes.byref(dims), _ptr(x), _ptr(Wg), _ptr(bg), _ptr(alive),
+                                 _ptr(idx), _ptr(w), _ptr(g), _ptr(scores), _ptr(ws),
+                                 _stream(stream)), "dmoe_gate_topk")
+
+
+def dmoe_dispatch(dims, x, idx, alive, counts, offsets, row_token, pos, x_perm, ws, stream=None):
+    _check(load().dmoe_dispatch(ctypes.byref(dims), _ptr(x), _ptr(idx), _ptr(alive), _ptr(counts),
+                                _ptr(offsets), _ptr(row_token), _ptr(pos), _ptr(x_perm), _ptr(ws),
+                                _stream(stream)), "dmoe_dispatch")
+
+
+def dmoe_expert_ffn_fwd(dims, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm, ws, stream=None):
+    _check(load().dmoe_expert_ffn_fwd(ctypes.byref(dims), _ptr(offsets), _ptr(x_perm), _ptr(W1),
+                                      _ptr(b1), _ptr(W2), _ptr(b2), _ptr(h), _ptr(a), _ptr(y_perm),
+                                      _ptr(ws), _stream(stream)), "dmoe_expert_ffn_fwd")
+
+
+def dmoe_combine(dims, y_perm, pos, w, y, stream=None):
+    _check(load().dmoe_combine(ctypes.byref(dims), _ptr(y_perm), _ptr(pos), _ptr(w), _ptr(y),
+                               _stream(stream)), "dmoe_combine")
+
+
+def dmoe_combine_bwd(dims, dy, y_perm, pos, w, dy_perm, dw, stream=None):
+    _check(load().dmoe_combine_bwd(ctypes.byref(dims), _ptr(dy), _ptr(y_perm), _ptr(pos), _ptr(w),
+                                   _ptr(dy_perm), _ptr(dw), _stream(stream)), "dmoe_combine_bwd")
+
+
+def dmoe_gate_topk_bwd(dims, x, idx, w, dw, alive, dg, dWg, dbg, ws, stream=None):
+    _check(load().dmoe_gate_topk_bwd(ctypes.byref(dims), _ptr(x), _ptr(idx), _ptr(w), _ptr(dw),
+                                     _ptr(alive), _ptr(dg), _ptr(dWg), _ptr(dbg), _ptr(ws),
+                                     _stream(stream)), "dmoe_gate_topk_bwd")
+
+
+def dmoe_expert_ffn_bwd(dims, offsets, counts, x_perm, h, a, dy_perm, W1, W2, dh, dx_perm, dW1, db1,
+                        dW2, db2, ws, stream=None):
+    _check(load().dmoe_expert_ffn_bwd(ctypes.byref(dims), _ptr(offsets), _ptr(counts), _ptr(x_perm),
+                                      _ptr(h), _ptr(a), _ptr(dy_perm), _ptr(W1), _ptr(W2), _ptr(dh),
+                                      _ptr(dx_perm), _ptr(dW1), _ptr(db1), _ptr(dW2), _ptr(db2),
+                                      _ptr(ws), _stream(stream)), "dmoe_expert_ffn_bwd")
+
+
+def dmoe_dispatch_bwd(dims, dx_perm, pos, idx, dg, Wg, dx, stream=None):
+    _check(load().dmoe_dispatch_bwd(ctypes.byref(dims), _ptr(dx_perm), _ptr(pos), _ptr(idx), _ptr(dg),
+                                    _ptr(Wg), _ptr(dx), _stream(stream)), "dmoe_dispatch_bwd")

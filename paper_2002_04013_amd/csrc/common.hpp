@@ -1,0 +1,127 @@
+// Shared device helpers of libdmoe: element types, bf16 rounding, MFMA wrappers,
+// launch checks and the workspace layout.  gfx950 (CDNA4), wave64.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "dmoe.h"
+
+namespace dmoe {
+
+typedef uint16_t bf16;   // bf16 storage (bit pattern)
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int KMAX = 8;          // largest k
+constexpr int DMAX = 4;          // largest grid dimensionality
+constexpr int DM_MAX = 128;      // largest d*M (gate columns)
+constexpr int NMAX = 16384;      // largest expert count (LDS histogram)
+constexpr int WAVE = 64;
+
+__device__ __forceinline__ float bf2f(bf16 v) { return __uint_as_float((uint32_t)v << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16)(u >> 16);
+}
+
+template <typename E> __device__ __forceinline__ float ldf(const E* p);
+template <> __device__ __forceinline__ float ldf<float>(const float* p) { return *p; }
+template <> __device__ __forceinline__ float ldf<bf16>(const bf16* p) { return bf2f(*p); }
+
+template <typename E> __device__ __forceinline__ E cvt(float v);
+template <> __device__ __forceinline__ float cvt<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 cvt<bf16>(float v) { return f2bf(v); }
+
+// 16-byte vector of elements <-> 16/sizeof(E) floats
+template <typename E> struct Vec;
+template <> struct Vec<float> {
+  static constexpr int N = 4;
+  __device__ static void unpack(const uint4& v, float* f) {
+    f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+  }
+  __device__ static uint4 pack(const float* f) {
+    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]),
+                      __float_as_uint(f[2]), __float_as_uint(f[3]));
+  }
+};
+template <> struct Vec<bf16> {
+  static constexpr int N = 8;
+  __device__ static void unpack(const uint4& v, float* f) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+  __device__ static uint4 pack(const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(f[2 * i]) | ((uint32_t)f2bf(f[2 * i + 1]) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+
+// Activations.  GELU is the erf form 0.5 h (1 + erf(h / sqrt 2)).
+__device__ __forceinline__ float act_fwd(float h, int act) {
+  if (act == DMOE_RELU) return h > 0.f ? h : 0.f;
+  return 0.5f * h * (1.f + erff(h * 0.70710678118654752f));
+}
+// derivative: ReLU' = [h > 0]; GELU' = Phi(h) + h phi(h)
+__device__ __forceinline__ float act_bwd(float h, int act) {
+  if (act == DMOE_RELU) return h > 0.f ? 1.f : 0.f;
+  const float phi = 0.39894228040143268f * __expf(-0.5f * h * h);
+  return 0.5f * (1.f + erff(h * 0.70710678118654752f)) + h * phi;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  return v;
+}
+
+// ----------------------------------------------------------------- host side
+
+struct Shape {
+  int64_t T, D, H, N, P, dM;
+  int d, M, k, dtype, act;
+  size_t esz;   // bytes per element of the layer dtype
+};
+
+int check_dims(const dmoe_dims* dims, Shape* s);
+
+inline int launch_status() {
+  return hipGetLastError() == hipSuccess ? DMOE_OK : DMOE_EHIP;
+}
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Workspace regions (byte offsets into the caller's ws buffer).
+struct Workspace {
+  size_t hist_off, hist_bytes;     // dispatch: per-block expert histograms
+  size_t tiles_off, tiles_bytes;   // grouped GEMM: tile prefix [N+1] + per-expert m-tiles
+  size_t ds_off, ds_bytes;         // gate backward: dense ds (bf16 hi/lo or fp32)
+  size_t part_off, part_bytes;     // gate backward: dWg partial sums per token split
+  size_t total;
+  int64_t disp_blocks;             // dispatch blocks (pairs per block = DISP_CHUNK)
+  int64_t gsplit, gsplit_tokens;   // gate backward token splits
+  int64_t ds_ld;                   // ds row stride (elements)
+};
+
+constexpr int DISP_CHUNK = 1024;   // pairs per dispatch block
+
+Workspace workspace_layout(const Shape& s);
+
+// Zero `bytes` bytes at p on stream st with a kernel (no hipMemsetAsync).
+void fill_zero(void* p, size_t bytes, hipStream_t st);
+
+}  // namespace dmoe

@@ -1,0 +1,268 @@
+// Expert feed-forward blocks on the per-expert row groups (the Runtime's batched
+// Forward and Backward of Sec. 3.3), as grouped GEMMs on MFMA.
+#include <algorithm>
+
+#include "common.hpp"
+#include "gemm.hpp"
+
+namespace dmoe {
+
+// tprefix[e] = tiles of experts before e:
+//   GROUP_M: ceil(rows_e / BM) * tiles_per;   GROUP_K: tiles_per if rows_e > 0.
+__global__ void __launch_bounds__(1024)
+tile_prep(const int32_t* offsets, int N, int mode, int BM, int tiles_per, int32_t* tprefix) {
+  __shared__ int sums[1024];
+  const int q = threadIdx.x;
+  const int EPT = (N + 1023) / 1024;
+  const int e0 = min(N, q * EPT), e1 = min(N, e0 + EPT);
+  int mine = 0;
+  for (int e = e0; e < e1; ++e) {
+    const int c = offsets[e + 1] - offsets[e];
+    mine += mode == GROUP_M ? (c + BM - 1) / BM * tiles_per : (c > 0 ? tiles_per : 0);
+  }
+  sums[q] = mine;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const int v = q >= o ? sums[q - o] : 0;
+    __syncthreads();
+    sums[q] += v;
+    __syncthreads();
+  }
+  int base = sums[q] - mine;
+  for (int e = e0; e < e1; ++e) {
+    tprefix[e] = base;
+    const int c = offsets[e + 1] - offsets[e];
+    base += mode == GROUP_M ? (c + BM - 1) / BM * tiles_per : (c > 0 ? tiles_per : 0);
+  }
+  if (q == 1023) tprefix[N] = sums[1023];
+}
+
+// out[e][c] = sum of rows [offsets[e], offsets[e+1]) of X[:, c]  (bias gradients);
+// experts without rows are skipped (their slots are left untouched).
+template <typename E>
+__global__ void __launch_bounds__(256)
+segment_colsum(const E* X, int64_t ld, const int32_t* offsets, int ncols, E* out) {
+  constexpr int VEC = 16 / sizeof(E);
+  const int e = blockIdx.y;
+  const int r0 = offsets[e], r1 = offsets[e + 1];
+  if (r1 == r0) return;
+  const int c = (blockIdx.x * 256 + threadIdx.x) * VEC;
+  if (c >= ncols) return;
+  float acc[VEC];
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
+  for (int r = r0; r < r1; ++r) {
+    float v[VEC];
+    Vec<E>::unpack(*reinterpret_cast<const uint4*>(X + (int64_t)r * ld + c), v);
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) acc[i] += v[i];
+  }
+  *reinterpret_cast<uint4*>(out + (int64_t)e * ncols + c) = Vec<E>::pack(acc);
+}
+
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  hipGetDevice(&dev);
+  if (dev < 0 || dev >= 64) return 256;
+  if (!cus[dev]) {
+    int v = 0;
+    hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev);
+    cus[dev] = v > 0 ? v : 256;
+  }
+  return cus[dev];
+}
+
+template <typename E, int GM, bool B_KC, int EPI, int BM, int BN, int BK, int WM, int WN>
+static void run_gemm(GemmArgs<E> p, int64_t tiles_ub, hipStream_t st) {
+  if (tiles_ub <= 0) return;
+  auto kern = grouped_gemm<E, GM, B_KC, EPI, BM, BN, BK, WM, WN>;
+  constexpr int NT = 64 * WM * WN;
+  const size_t lds = gemm_lds_bytes<E, BM, BN, BK, WM, WN>();
+  static int per_cu = 0;
+  if (!per_cu) {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, NT, lds) != hipSuccess || nb < 1) nb = 1;
+    per_cu = nb;
+  }
+  const int64_t resident = (int64_t)per_cu * device_cus();
+  const int grid = (int)std::min<int64_t>(tiles_ub, resident);
+  p.chunked = grid >= 8;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
+}
+
+template <typename E>
+static GemmArgs<E> args_m(const int32_t* offsets, const int32_t* tpre, int N) {
+  GemmArgs<E> p{};
+  p.offsets = offsets; p.tprefix = tpre; p.groups = N;
+  return p;
+}
+
+// Tile shapes.  bf16: few rows per expert -> 32-row tiles that stream the weights
+// (256 weight rows per tile); many rows -> 128x128 tiles.  fp32: small tiles.
+struct CfgSkinny { static constexpr int BM = 32, BN = 256, BK = 32, WM = 1, WN = 4; };
+struct CfgFat    { static constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2; };
+struct CfgF32    { static constexpr int BM = 32, BN = 64, BK = 32, WM = 1, WN = 2; };
+struct CfgDW     { static constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2; };
+struct CfgDWF32  { static constexpr int BM = 64, BN = 64, BK = 32, WM = 2, WN = 2; };
+
+template <typename E, typename C>
+static void ffn_fwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, const E* W1,
+                        const E* b1, const E* W2, const E* b2, E* h, E* a, E* yp, int32_t* tpre,
+                        hipStream_t st) {
+  const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
+  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  // h = x W1^T + b1, a = act(h)
+  {
+    const int nt = (H + C::BN - 1) / C::BN;
+    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_M, C::BM, nt, tpre);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    p.A = xp; p.lda = D;
+    p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
+    p.C = h; p.ldc = H; p.C2 = a;
+    p.bias = b1; p.bias_gstride = H;
+    p.N = H; p.K = D; p.act = s.act;
+    run_gemm<E, GROUP_M, true, EPI_BIAS_ACT, C::BM, C::BN, C::BK, C::WM, C::WN>(p, mt_ub * nt, st);
+  }
+  // y = a W2^T + b2
+  {
+    const int nt = (D + C::BN - 1) / C::BN;
+    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_M, C::BM, nt, tpre);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    p.A = a; p.lda = H;
+    p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
+    p.C = yp; p.ldc = D;
+    p.bias = b2; p.bias_gstride = D;
+    p.N = D; p.K = H; p.act = s.act;
+    run_gemm<E, GROUP_M, true, EPI_BIAS, C::BM, C::BN, C::BK, C::WM, C::WN>(p, mt_ub * nt, st);
+  }
+}
+
+template <typename E, typename C, typename CW>
+static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, const E* h,
+                        const E* a, const E* dyp, const E* W1, const E* W2, E* dh, E* dxp, E* dW1,
+                        E* db1, E* dW2, E* db2, int32_t* tpre, hipStream_t st) {
+  const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
+  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  const int64_t active_ub = std::min<int64_t>(s.N, s.P);
+  // dh = (dy W2) * act'(h)       B = W2_e viewed as (n = h, k = d): N-contiguous
+  {
+    const int nt = (H + C::BN - 1) / C::BN;
+    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_M, C::BM, nt, tpre);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    p.A = dyp; p.lda = D;
+    p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
+    p.C = dh; p.ldc = H; p.aux = h;
+    p.N = H; p.K = D; p.act = s.act;
+    run_gemm<E, GROUP_M, false, EPI_DACT, C::BM, C::BN, C::BK, C::WM, C::WN>(p, mt_ub * nt, st);
+  }
+  // dW2_e = dy_e^T a_e   [D, H]
+  {
+    const int mt = (D + CW::BM - 1) / CW::BM, nt = (H + CW::BN - 1) / CW::BN;
+    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_K, 0, mt * nt, tpre);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    p.A = dyp; p.lda = D;
+    p.B = a; p.ldb = H;
+    p.C = dW2; p.ldc = H; p.c_gstride = (int64_t)D * H;
+    p.M = D; p.N = H; p.act = s.act;
+    run_gemm<E, GROUP_K, false, EPI_STORE, CW::BM, CW::BN, CW::BK, CW::WM, CW::WN>(p, active_ub * mt * nt, st);
+  }
+  // dx_perm = dh W1              B = W1_e viewed as (n = d, k = h): N-contiguous
+  {
+    const int nt = (D + C::BN - 1) / C::BN;
+    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_M, C::BM, nt, tpre);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    p.A = dh; p.lda = H;
+    p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
+    p.C = dxp; p.ldc = D;
+    p.N = D; p.K = H; p.act = s.act;
+    run_gemm<E, GROUP_M, false, EPI_STORE, C::BM, C::BN, C::BK, C::WM, C::WN>(p, mt_ub * nt, st);
+  }
+  // dW1_e = dh_e^T x_e   [H, D]
+  {
+    const int mt = (H + CW::BM - 1) / CW::BM, nt = (D + CW::BN - 1) / CW::BN;
+    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_K, 0, mt * nt, tpre);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    p.A = dh; p.lda = H;
+    p.B = xp; p.ldb = D;
+    p.C = dW1; p.ldc = D; p.c_gstride = (int64_t)H * D;
+    p.M = H; p.N = D; p.act = s.act;
+    run_gemm<E, GROUP_K, false, EPI_STORE, CW::BM, CW::BN, CW::BK, CW::WM, CW::WN>(p, active_ub * mt * nt, st);
+  }
+  // bias gradients
+  constexpr int VEC = 16 / sizeof(E);
+  hipLaunchKernelGGL(segment_colsum<E>, dim3((unsigned)((H / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
+                     st, dh, (int64_t)H, offsets, H, db1);
+  hipLaunchKernelGGL(segment_colsum<E>, dim3((unsigned)((D / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
+                     st, dyp, (int64_t)D, offsets, D, db2);
+}
+
+static bool use_fat(const Shape& s) { return s.P >= (int64_t)96 * s.N; }
+
+}  // namespace dmoe
+
+using namespace dmoe;
+
+extern "C" int dmoe_expert_ffn_fwd(const dmoe_dims* dims, const int32_t* offsets, const void* x_perm,
+                                   const void* W1, const void* b1, const void* W2, const void* b2,
+                                   void* h, void* a, void* y_perm, void* ws, void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s);
+  if (rc) return rc;
+  if (s.T == 0) return DMOE_OK;
+  if (!offsets || !x_perm || !W1 || !b1 || !W2 || !b2 || !h || !a || !y_perm || !ws) return DMOE_EINVAL;
+  for (const void* q : {x_perm, W1, W2, (const void*)h, (const void*)a, (const void*)y_perm, (const void*)ws})
+    if (!aligned16(q)) return DMOE_EUNSUPPORTED;
+  const Workspace L = workspace_layout(s);
+  int32_t* tpre = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + L.tiles_off);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (s.dtype == DMOE_BF16) {
+    auto c = [](const void* q) { return reinterpret_cast<const bf16*>(q); };
+    auto m = [](void* q) { return reinterpret_cast<bf16*>(q); };
+    if (use_fat(s))
+      ffn_fwd_cfg<bf16, CfgFat>(s, offsets, c(x_perm), c(W1), c(b1), c(W2), c(b2), m(h), m(a), m(y_perm), tpre, st);
+    else
+      ffn_fwd_cfg<bf16, CfgSkinny>(s, offsets, c(x_perm), c(W1), c(b1), c(W2), c(b2), m(h), m(a), m(y_perm), tpre, st);
+  } else {
+    auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };
+    auto m = [](void* q) { return reinterpret_cast<float*>(q); };
+    ffn_fwd_cfg<float, CfgF32>(s, offsets, c(x_perm), c(W1), c(b1), c(W2), c(b2), m(h), m(a), m(y_perm), tpre, st);
+  }
+  return launch_status();
+}
+
+extern "C" int dmoe_expert_ffn_bwd(const dmoe_dims* dims, const int32_t* offsets, const int32_t* counts,
+                                   const void* x_perm, const void* h, const void* a, const void* dy_perm,
+                                   const void* W1, const void* W2, void* dh, void* dx_perm, void* dW1,
+                                   void* db1, void* dW2, void* db2, void* ws, void* stream) {
+  (void)counts;
+  Shape s;
+  int rc = check_dims(dims, &s);
+  if (rc) return rc;
+  if (s.T == 0) return DMOE_OK;
+  if (!offsets || !x_perm || !h || !a || !dy_perm || !W1 || !W2 || !dh || !dx_perm || !dW1 || !db1 ||
+      !dW2 || !db2 || !ws)
+    return DMOE_EINVAL;
+  for (const void* q : {x_perm, h, a, dy_perm, W1, W2, (const void*)dh, (const void*)dx_perm,
+                        (const void*)dW1, (const void*)db1, (const void*)dW2, (const void*)db2, (const void*)ws})
+    if (!aligned16(q)) return DMOE_EUNSUPPORTED;
+  const Workspace L = workspace_layout(s);
+  int32_t* tpre = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + L.tiles_off);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (s.dtype == DMOE_BF16) {
+    auto c = [](const void* q) { return reinterpret_cast<const bf16*>(q); };
+    auto m = [](void* q) { return reinterpret_cast<bf16*>(q); };
+    if (use_fat(s))
+      ffn_bwd_cfg<bf16, CfgFat, CfgDW>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
+                                       m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
+    else
+      ffn_bwd_cfg<bf16, CfgSkinny, CfgDW>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
+                                          m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
+  } else {
+    auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };
+    auto m = [](void* q) { return reinterpret_cast<float*>(q); };
+    ffn_bwd_cfg<float, CfgF32, CfgDWF32>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
+                                         m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
+  }
+  return launch_status();
+}

@@ -1,0 +1,335 @@
+// Dispatch of (token, expert) pairs into per-expert row groups, the weighted
+// combine of Eq. 1, and their backward passes.
+//
+// Dispatch is a stable counting sort by expert, without atomics on row order:
+//   1. per block of DISP_CHUNK pairs, an LDS histogram of alive pairs per expert;
+//   2. one block turns the histograms into counts, offsets (exclusive scan) and
+//      each block's starting row per expert;
+//   3. each block ranks its pairs within every expert in pair order (wave-wide
+//      rank by lane comparison, waves taken in order) and writes pos/row_token;
+//   4. rows of x are gathered into x_perm with 16-byte vector copies.
+#include "common.hpp"
+
+namespace dmoe {
+
+constexpr int RT_NT = 256;
+
+__global__ void __launch_bounds__(RT_NT)
+dispatch_hist(const int32_t* idx, const uint8_t* alive, int P, int N, int32_t* block_hist) {
+  extern __shared__ int hist[];
+  for (int e = threadIdx.x; e < N; e += RT_NT) hist[e] = 0;
+  __syncthreads();
+  const int p0 = blockIdx.x * DISP_CHUNK;
+  const int p1 = min(P, p0 + DISP_CHUNK);
+  for (int p = p0 + threadIdx.x; p < p1; p += RT_NT) {
+    const int e = idx[p];
+    if (alive == nullptr || alive[e]) atomicAdd(&hist[e], 1);
+  }
+  __syncthreads();
+  int32_t* out = block_hist + (int64_t)blockIdx.x * N;
+  for (int e = threadIdx.x; e < N; e += RT_NT) out[e] = hist[e];
+}
+
+// One block of 1024 threads; thread q owns experts [q*EPT, (q+1)*EPT).
+__global__ void __launch_bounds__(1024)
+dispatch_scan(int32_t* block_hist, int nb, int N, int32_t* counts, int32_t* offsets) {
+  __shared__ int sums[1024];
+  const int q = threadIdx.x;
+  const int EPT = (N + 1023) / 1024;
+  const int e0 = min(N, q * EPT), e1 = min(N, e0 + EPT);
+  int mine = 0;
+  for (int e = e0; e < e1; ++e) {
+    int run = 0;
+    for (int b = 0; b < nb; ++b) {
+      int32_t* h = block_hist + (int64_t)b * N + e;
+      const int c = *h;
+      *h = run;
+      run += c;
+    }
+    counts[e] = run;
+    mine += run;
+  }
+  sums[q] = mine;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {     // inclusive Hillis-Steele scan
+    const int v = q >= o ? sums[q - o] : 0;
+    __syncthreads();
+    sums[q] += v;
+    __syncthreads();
+  }
+  int base = sums[q] - mine;
+  for (int e = e0; e < e1; ++e) {
+    offsets[e] = base;
+    for (int b = 0; b < nb; ++b) block_hist[(int64_t)b * N + e] += base;
+    base += counts[e];
+  }
+  if (q == 1023) offsets[N] = sums[1023];
+}
+
+__global__ void __launch_bounds__(RT_NT)
+dispatch_scatter(const int32_t* idx, const uint8_t* alive, int P, int N, int k,
+                 const int32_t* block_hist, int32_t* pos, int32_t* row_token) {
+  extern __shared__ int base[];
+  const int32_t* bh = block_hist + (int64_t)blockIdx.x * N;
+  for (int e = threadIdx.x; e < N; e += RT_NT) base[e] = bh[e];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int r = 0; r < DISP_CHUNK / RT_NT; ++r) {
+    const int p = blockIdx.x * DISP_CHUNK + r * RT_NT + threadIdx.x;
+    int e = -1;
+    if (p < P) {
+      const int e0 = idx[p];
+      if (alive == nullptr || alive[e0]) e = e0;
+    }
+    int rank = 0;
+    bool last = true;
+    for (int s = 0; s < 64; ++s) {
+      const int o = __builtin_amdgcn_readlane(e, s);
+      if (o == e) {
+        rank += s < lane;
+        last = last && !(s > lane);
+      }
+    }
+    int row = -1;
+    for (int w = 0; w < RT_NT / 64; ++w) {
+      if (wave == w && e >= 0) {
+        row = base[e] + rank;
+        if (last) base[e] = row + 1;
+      }
+      __syncthreads();
+    }
+    if (p < P) {
+      pos[p] = row;
+      if (row >= 0) row_token[row] = p / k;
+    }
+  }
+}
+
+template <typename E>
+__global__ void __launch_bounds__(RT_NT)
+gather_rows(const E* x, const int32_t* row_token, const int32_t* offsets, int N, int D, E* xp) {
+  constexpr int VEC = 16 / sizeof(E);
+  const int CPR = D / VEC;
+  const int64_t total = (int64_t)offsets[N] * CPR;
+  for (int64_t q = (int64_t)blockIdx.x * RT_NT + threadIdx.x; q < total; q += (int64_t)gridDim.x * RT_NT) {
+    const int64_t r = q / CPR;
+    const int c = (int)(q % CPR);
+    const int t = row_token[r];
+    *reinterpret_cast<uint4*>(xp + r * D + c * VEC) =
+        *reinterpret_cast<const uint4*>(x + (int64_t)t * D + c * VEC);
+  }
+}
+
+// y[t] = sum_j w[t,j] y_perm[pos[t,j]]; one wave per token.
+template <typename E>
+__global__ void __launch_bounds__(RT_NT)
+combine_kernel(const E* yp, const int32_t* pos, const float* w, E* y, int T, int D, int k) {
+  constexpr int VEC = 16 / sizeof(E);
+  const int t = blockIdx.x * (RT_NT / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= T) return;
+  int pj[KMAX];
+  float wj[KMAX];
+  for (int j = 0; j < k; ++j) {
+    pj[j] = pos[(int64_t)t * k + j];
+    wj[j] = w[(int64_t)t * k + j];
+  }
+  const int CPR = D / VEC;
+  for (int c = lane; c < CPR; c += 64) {
+    float acc[VEC];
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
+    for (int j = 0; j < k; ++j) {
+      if (pj[j] < 0) continue;
+      float v[VEC];
+      Vec<E>::unpack(*reinterpret_cast<const uint4*>(yp + (int64_t)pj[j] * D + c * VEC), v);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) acc[i] = fmaf(wj[j], v[i], acc[i]);
+    }
+    *reinterpret_cast<uint4*>(y + (int64_t)t * D + c * VEC) = Vec<E>::pack(acc);
+  }
+}
+
+// dy_perm[pos[t,j]] = w[t,j] dy[t];  dw[t,j] = <dy[t], y_perm[pos[t,j]]>
+template <typename E>
+__global__ void __launch_bounds__(RT_NT)
+combine_bwd_kernel(const E* dy, const E* yp, const int32_t* pos, const float* w, E* dyp,
+                   float* dw, int T, int D, int k) {
+  constexpr int VEC = 16 / sizeof(E);
+  const int t = blockIdx.x * (RT_NT / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= T) return;
+  int pj[KMAX];
+  float wj[KMAX], dot[KMAX];
+  for (int j = 0; j < k; ++j) {
+    pj[j] = pos[(int64_t)t * k + j];
+    wj[j] = w[(int64_t)t * k + j];
+    dot[j] = 0.f;
+  }
+  const int CPR = D / VEC;
+  for (int c = lane; c < CPR; c += 64) {
+    float g[VEC];
+    Vec<E>::unpack(*reinterpret_cast<const uint4*>(dy + (int64_t)t * D + c * VEC), g);
+    for (int j = 0; j < k; ++j) {
+      if (pj[j] < 0) continue;
+      float v[VEC], o[VEC];
+      Vec<E>::unpack(*reinterpret_cast<const uint4*>(yp + (int64_t)pj[j] * D + c * VEC), v);
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        s = fmaf(g[i], v[i], s);
+        o[i] = wj[j] * g[i];
+      }
+      dot[j] += s;
+      *reinterpret_cast<uint4*>(dyp + (int64_t)pj[j] * D + c * VEC) = Vec<E>::pack(o);
+    }
+  }
+  for (int j = 0; j < k; ++j) {
+    const float s = wave_sum(dot[j]);
+    if (lane == 0) dw[(int64_t)t * k + j] = pj[j] >= 0 ? s : 0.f;
+  }
+}
+
+// dx[t] = sum_j dx_perm[pos[t,j]]  (+ sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])])
+template <typename E>
+__global__ void __launch_bounds__(RT_NT)
+dispatch_bwd_kernel(const E* dxp, const int32_t* pos, const int32_t* idx, const float* dg,
+                    const E* Wg, E* dx, int T, int D, int k, int d, int M) {
+  constexpr int VEC = 16 / sizeof(E);
+  const int t = blockIdx.x * (RT_NT / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= T) return;
+  int pj[KMAX];
+  for (int j = 0; j < k; ++j) pj[j] = pos[(int64_t)t * k + j];
+  const bool gate = dg != nullptr;
+  const int CPR = D / VEC;
+  for (int c = lane; c < CPR; c += 64) {
+    float acc[VEC];
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
+    for (int j = 0; j < k; ++j) {
+      if (pj[j] < 0) continue;
+      float v[VEC];
+      Vec<E>::unpack(*reinterpret_cast<const uint4*>(dxp + (int64_t)pj[j] * D + c * VEC), v);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) acc[i] += v[i];
+    }
+    if (gate) {
+      for (int j = 0; j < k; ++j) {
+        const float gj = dg[(int64_t)t * k + j];
+        int rem = idx[(int64_t)t * k + j];
+        for (int i = d - 1; i >= 0; --i) {
+          const int col = i * M + rem % M;
+          rem /= M;
+          float v[VEC];
+          Vec<E>::unpack(*reinterpret_cast<const uint4*>(Wg + (int64_t)col * D + c * VEC), v);
+#pragma unroll
+          for (int q = 0; q < VEC; ++q) acc[q] = fmaf(gj, v[q], acc[q]);
+        }
+      }
+    }
+    *reinterpret_cast<uint4*>(dx + (int64_t)t * D + c * VEC) = Vec<E>::pack(acc);
+  }
+}
+
+}  // namespace dmoe
+
+using namespace dmoe;
+
+extern "C" int dmoe_dispatch(const dmoe_dims* dims, const void* x, const int32_t* idx,
+                             const uint8_t* alive, int32_t* counts, int32_t* offsets,
+                             int32_t* row_token, int32_t* pos, void* x_perm, void* ws,
+                             void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s);
+  if (rc) return rc;
+  if (!counts || !offsets || !ws || (s.T > 0 && (!x || !idx || !row_token || !pos || !x_perm)))
+    return DMOE_EINVAL;
+  if (!aligned16(ws) || (s.T > 0 && (!aligned16(x) || !aligned16(x_perm)))) return DMOE_EUNSUPPORTED;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const Workspace L = workspace_layout(s);
+  int32_t* bh = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + L.hist_off);
+  const int N = (int)s.N, P = (int)s.P;
+  const int nb = (int)L.disp_blocks;
+  if (nb > 0)
+    hipLaunchKernelGGL(dispatch_hist, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N, bh);
+  hipLaunchKernelGGL(dispatch_scan, dim3(1), dim3(1024), 0, st, bh, nb, N, counts, offsets);
+  if (nb == 0) return launch_status();
+  hipLaunchKernelGGL(dispatch_scatter, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N,
+                     s.k, bh, pos, row_token);
+  const int64_t chunks = s.P * (s.D * (int64_t)s.esz / 16);
+  const int grid = (int)std::min<int64_t>((chunks + RT_NT - 1) / RT_NT, 256 * 16);
+  if (s.dtype == DMOE_BF16)
+    hipLaunchKernelGGL(gather_rows<bf16>, dim3(grid), dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(x),
+                       row_token, offsets, N, (int)s.D, reinterpret_cast<bf16*>(x_perm));
+  else
+    hipLaunchKernelGGL(gather_rows<float>, dim3(grid), dim3(RT_NT), 0, st, reinterpret_cast<const float*>(x),
+                       row_token, offsets, N, (int)s.D, reinterpret_cast<float*>(x_perm));
+  return launch_status();
+}
+
+extern "C" int dmoe_combine(const dmoe_dims* dims, const void* y_perm, const int32_t* pos,
+                            const float* w, void* y, void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s);
+  if (rc) return rc;
+  if (s.T == 0) return DMOE_OK;
+  if (!y_perm || !pos || !w || !y) return DMOE_EINVAL;
+  if (!aligned16(y_perm) || !aligned16(y)) return DMOE_EUNSUPPORTED;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const dim3 grid((unsigned)((s.T + 3) / 4));
+  if (s.dtype == DMOE_BF16)
+    hipLaunchKernelGGL(combine_kernel<bf16>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(y_perm),
+                       pos, w, reinterpret_cast<bf16*>(y), (int)s.T, (int)s.D, s.k);
+  else
+    hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const float*>(y_perm),
+                       pos, w, reinterpret_cast<float*>(y), (int)s.T, (int)s.D, s.k);
+  return launch_status();
+}
+
+extern "C" int dmoe_combine_bwd(const dmoe_dims* dims, const void* dy, const void* y_perm,
+                                const int32_t* pos, const float* w, void* dy_perm, float* dw,
+                                void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s);
+  if (rc) return rc;
+  if (s.T == 0) return DMOE_OK;
+  if (!dy || !y_perm || !pos || !w || !dy_perm || !dw) return DMOE_EINVAL;
+  if (!aligned16(dy) || !aligned16(y_perm) || !aligned16(dy_perm)) return DMOE_EUNSUPPORTED;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const dim3 grid((unsigned)((s.T + 3) / 4));
+  if (s.dtype == DMOE_BF16)
+    hipLaunchKernelGGL(combine_bwd_kernel<bf16>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(dy),
+                       reinterpret_cast<const bf16*>(y_perm), pos, w, reinterpret_cast<bf16*>(dy_perm), dw,
+                       (int)s.T, (int)s.D, s.k);
+  else
+    hipLaunchKernelGGL(combine_bwd_kernel<float>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const float*>(dy),
+                       reinterpret_cast<const float*>(y_perm), pos, w, reinterpret_cast<float*>(dy_perm), dw,
+                       (int)s.T, (int)s.D, s.k);
+  return launch_status();
+}
+
+extern "C" int dmoe_dispatch_bwd(const dmoe_dims* dims, const void* dx_perm, const int32_t* pos,
+                                 const int32_t* idx, const float* dg, const void* Wg, void* dx,
+                                 void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s);
+  if (rc) return rc;
+  if (s.T == 0) return DMOE_OK;
+  if (!dx_perm || !pos || !dx) return DMOE_EINVAL;
+  const bool gate = idx && dg && Wg;
+  if (!aligned16(dx_perm) || !aligned16(dx) || (gate && !aligned16(Wg))) return DMOE_EUNSUPPORTED;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const dim3 grid((unsigned)((s.T + 3) / 4));
+  if (s.dtype == DMOE_BF16)
+    hipLaunchKernelGGL(dispatch_bwd_kernel<bf16>, grid, dim3(RT_NT), 0, st,
+                       reinterpret_cast<const bf16*>(dx_perm), pos, gate ? idx : nullptr, gate ? dg : nullptr,
+                       reinterpret_cast<const bf16*>(Wg), reinterpret_cast<bf16*>(dx), (int)s.T, (int)s.D, s.k,
+                       s.d, s.M);
+  else
+    hipLaunchKernelGGL(dispatch_bwd_kernel<float>, grid, dim3(RT_NT), 0, st,
+                       reinterpret_cast<const float*>(dx_perm), pos, gate ? idx : nullptr, gate ? dg : nullptr,
+                       reinterpret_cast<const float*>(Wg), reinterpret_cast<float*>(dx), (int)s.T, (int)s.D, s.k,
+                       s.d, s.M);
+  return launch_status();
+}

@@ -1,0 +1,70 @@
+"""One DMoE layer on one GPU: buffers (torch.empty on the device) and the order of
+the C-ABI calls for the forward and the backward pass.
+
+Forward:  gate_topk -> dispatch -> expert_ffn_fwd -> combine
+Backward: combine_bwd -> gate_topk_bwd -> expert_ffn_bwd -> dispatch_bwd
+"""
+import torch
+
+from . import abi
+
+
+class DMoELayer:
+    """Device buffers for one layer shape; parameters are passed per call."""
+
+    def __init__(self, T, D, H, d, M, k, dtype="bf16", act="gelu", device="cuda",
+                 dh_aliases_h=False):
+        self.dims = abi.make_dims(T, D, H, d, M, k, dtype, act)
+        self.T, self.D, self.H, self.d, self.M, self.k = T, D, H, d, M, k
+        self.N = M ** d
+        self.P = T * k
+        self.dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        dev = torch.device(device)
+        e = lambda *s, dt=None: torch.empty(s, dtype=dt or self.dt, device=dev)
+        i32 = torch.int32
+        nws = abi.workspace_bytes(self.dims)
+        if nws == 0:
+            raise abi.DmoeError("unsupported layer shape")
+        self.ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+        P, N = self.P, self.N
+        self.idx = e(T, k, dt=i32)
+        self.w = e(T, k, dt=torch.float32)
+        self.g = e(T, k, dt=torch.float32)
+        self.scores = e(T, d * M, dt=torch.float32)
+        self.counts = e(N, dt=i32)
+        self.offsets = e(N + 1, dt=i32)
+        self.row_token = e(max(P, 1), dt=i32)
+        self.pos = e(T, k, dt=i32)
+        self.x_perm = e(max(P, 1), D)
+        self.h = e(max(P, 1), H)
+        self.a = e(max(P, 1), H)
+        self.y_perm = e(max(P, 1), D)
+        self.y = e(T, D)
+        # backward
+        self.dy_perm = e(max(P, 1), D)
+        self.dw = e(T, k, dt=torch.float32)
+        self.dg = e(T, k, dt=torch.float32)
+        self.dh = self.h if dh_aliases_h else e(max(P, 1), H)
+        self.dx_perm = e(max(P, 1), D)
+        self.dx = e(T, D)
+
+    def forward(self, x, Wg, bg, alive, W1, b1, W2, b2, scores=True):
+        D = self.dims
+        abi.dmoe_gate_topk(D, x, Wg, bg, alive, self.idx, self.w, self.g,
+                           self.scores if scores else None, self.ws)
+        abi.dmoe_dispatch(D, x, self.idx, alive, self.counts, self.offsets, self.row_token,
+                          self.pos, self.x_perm, self.ws)
+        abi.dmoe_expert_ffn_fwd(D, self.offsets, self.x_perm, W1, b1, W2, b2, self.h, self.a,
+                                self.y_perm, self.ws)
+        abi.dmoe_combine(D, self.y_perm, self.pos, self.w, self.y)
+        return self.y
+
+    def backward(self, dy, x, Wg, alive, W1, W2, dW1, db1, dW2, db2, dWg, dbg):
+        D = self.dims
+        abi.dmoe_combine_bwd(D, dy, self.y_perm, self.pos, self.w, self.dy_perm, self.dw)
+        abi.dmoe_gate_topk_bwd(D, x, self.idx, self.w, self.dw, alive, self.dg, dWg, dbg, self.ws)
+        abi.dmoe_expert_ffn_bwd(D, self.offsets, self.counts, self.x_perm, self.h, self.a,
+                                self.dy_perm, W1, W2, self.dh, self.dx_perm, dW1, db1, dW2, db2,
+                                self.ws)
+        abi.dmoe_dispatch_bwd(D, self.dx_perm, self.pos, self.idx, self.dg, Wg, self.dx)
+        return self.dx

@@ -1,0 +1,120 @@
+"""Helpers of the GPU parity tests: run the HIP path through the C ABI and the
+oracle on the same seeded inputs, and compare them."""
+import sys
+
+import numpy as np
+import torch
+
+import oracle as O
+from workloads import make_inputs
+
+RTOL = {"bf16": 2e-2, "f32": 1e-5}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def assert_close(gpu, ref, rtol, name):
+    """|gpu - ref| <= rtol * (|ref| + rms(ref)), elementwise."""
+    g = O.to64(gpu)
+    r = np.asarray(ref, np.float64)
+    assert g.shape == r.shape, (name, g.shape, r.shape)
+    if r.size == 0:
+        return
+    assert np.isfinite(g).all(), f"{name}: non-finite values"
+    rms = float(np.sqrt(np.mean(r * r)))
+    err = np.abs(g - r)
+    lim = rtol * (np.abs(r) + rms) + 1e-30
+    bad = err > lim
+    if bad.any():
+        i = np.unravel_index(np.argmax(err / lim), err.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())}/{bad.size} out of tolerance; worst at {i}: "
+                             f"gpu {g[i]!r} ref {r[i]!r} (rtol {rtol}, rms {rms:.3g})")
+
+
+def gpu_run(wl, inp, backward=True, dh_aliases_h=False):
+    """Forward (and backward) through the C ABI on cuda:0; returns CPU copies."""
+    from paper_2002_04013_amd import DMoELayer
+    dev = torch.device("cuda")
+    t = {n: v.to(dev) for n, v in inp.items()}
+    L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, dh_aliases_h=dh_aliases_h)
+    out = {}
+    L.forward(t["x"], t["Wg"], t["bg"], t["alive"], t["W1"], t["b1"], t["W2"], t["b2"])
+    if backward:
+        dt = L.dt
+        sentinel = 7.0
+        dW1 = torch.full_like(t["W1"], sentinel)
+        db1 = torch.full_like(t["b1"], sentinel)
+        dW2 = torch.full_like(t["W2"], sentinel)
+        db2 = torch.full_like(t["b2"], sentinel)
+        dWg = torch.empty_like(t["Wg"])
+        dbg = torch.empty_like(t["bg"])
+        L.backward(t["dy"], t["x"], t["Wg"], t["alive"], t["W1"], t["W2"], dW1, db1, dW2, db2, dWg, dbg)
+        out.update(dW1=dW1, db1=db1, dW2=dW2, db2=db2, dWg=dWg, dbg=dbg, dx=L.dx, dw=L.dw, dg=L.dg,
+                   dy_perm=L.dy_perm, dx_perm=L.dx_perm, dh=L.dh)
+    torch.cuda.synchronize()
+    out.update(idx=L.idx, w=L.w, g=L.g, scores=L.scores, counts=L.counts, offsets=L.offsets,
+               row_token=L.row_token, pos=L.pos, x_perm=L.x_perm, h=L.h, a=L.a, y_perm=L.y_perm, y=L.y)
+    return {k: v.detach().cpu() for k, v in out.items()}
+
+
+def oracle_run(wl, inp, backward=True):
+    f = {n: O.to64(v) for n, v in inp.items() if n != "alive"}
+    alive = inp["alive"].cpu().numpy()
+    ex = (f["W1"], f["b1"], f["W2"], f["b2"])
+    # a bf16 layer keeps h, a, expert outputs and their row gradients in bf16
+    store = O.round_bf16 if wl.dtype == "bf16" else None
+    fwd = O.layer_forward(f["x"], f["Wg"], f["bg"], ex, alive, wl.d, wl.M, wl.k, wl.act, store=store)
+    bwd = O.layer_backward(fwd, f["dy"], f["x"], f["Wg"], ex, alive, wl.d, wl.M, wl.k, wl.act,
+                           store=store) if backward else None
+    return fwd, bwd
+
+
+def compare(wl, inp, gpu, fwd, bwd):
+    """Full comparison of one run: integers bit-exact, floats to the tolerance."""
+    rtol = RTOL[wl.dtype]
+    T, k, N = wl.T, wl.k, wl.N
+    # gate scores: fp64 accumulation then one fp32 rounding -> within 1 ulp of exact
+    S = fwd["S"]
+    sc = O.to64(gpu["scores"])
+    assert np.all(np.abs(sc - S) <= np.abs(S) * 2.0 ** -23 + 1e-30), "scores"
+    # TopK: bit-exact set and order
+    np.testing.assert_array_equal(gpu["idx"].numpy(), fwd["idx"], "idx")
+    np.testing.assert_allclose(gpu["w"].numpy(), fwd["w"], rtol=1e-6, atol=1e-6, err_msg="w")
+    np.testing.assert_allclose(gpu["g"].numpy(), fwd["g"], rtol=1e-6, atol=1e-6, err_msg="g")
+    # dispatch: exact
+    np.testing.assert_array_equal(gpu["counts"].numpy(), fwd["counts"], "counts")
+    np.testing.assert_array_equal(gpu["offsets"].numpy(), fwd["offsets"], "offsets")
+    rows = int(fwd["offsets"][-1])
+    np.testing.assert_array_equal(gpu["row_token"].numpy()[:rows], fwd["row_token"], "row_token")
+    np.testing.assert_array_equal(gpu["pos"].numpy(), fwd["pos"], "pos")
+    xp = gpu["x_perm"][:rows]
+    assert torch.equal(xp, inp["x"][torch.from_numpy(fwd["row_token"]).long()]), "x_perm"
+    if rows:
+        assert_close(gpu["h"][:rows], fwd["h"], rtol, "h")
+        assert_close(gpu["a"][:rows], fwd["a"], rtol, "a")
+        assert_close(gpu["y_perm"][:rows], fwd["y_perm"], rtol, "y_perm")
+    assert_close(gpu["y"], fwd["y"], rtol, "y")
+    if bwd is None:
+        return
+    assert_close(gpu["dw"], bwd["dw"], rtol, "dw")
+    assert_close(gpu["dg"], bwd["dg"], rtol, "dg")
+    if rows:
+        assert_close(gpu["dy_perm"][:rows], bwd["dy_perm"], rtol, "dy_perm")
+        assert_close(gpu["dx_perm"][:rows], bwd["dx_perm"], rtol, "dx_perm")
+    assert_close(gpu["dx"], bwd["dx"], rtol, "dx")
+    assert_close(gpu["dWg"], bwd["dWg"], rtol, "dWg")
+    assert_close(gpu["dbg"], bwd["dbg"], rtol, "dbg")
+    counts = fwd["counts"]
+    for e in range(N):
+        if counts[e] > 0:
+            dW1, db1, dW2, db2 = bwd["expert_grads"][e]
+            assert_close(gpu["dW1"][e], dW1, rtol, f"dW1[{e}]")
+            assert_close(gpu["db1"][e], db1, rtol, f"db1[{e}]")
+            assert_close(gpu["dW2"][e], dW2, rtol, f"dW2[{e}]")
+            assert_close(gpu["db2"][e], db2, rtol, f"db2[{e}]")
+        else:   # untouched experts keep the caller's contents
+            for n in ("dW1", "db1", "dW2", "db2"):
+                assert bool((gpu[n][e].float() == 7.0).all()), f"{n}[{e}] was written"

@@ -1,0 +1,143 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle, element by
+element, on seeded inputs small enough for the oracle to finish in seconds while
+still spanning several GEMM tiles and ragged tails."""
+import numpy as np
+import pytest
+import torch
+
+from parity_util import assert_close, compare, gpu_run, oracle_run, say
+from workloads import Workload, make_inputs, small_workload
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # the tiny fp32 workload exactly as named (64 tokens, 4x4 grid, top-2, ReLU)
+    "tiny_f32": small_workload("tiny_f32"),
+    # bf16, skinny experts (few rows each): 32-row GEMM tiles, ragged rows, dead experts
+    "bf16_skinny": Workload("bf16_skinny", 10, T=512, D=256, H=512, d=2, M=8, k=4, dtype="bf16",
+                            act="gelu", p_alive=0.8),
+    # bf16, fat experts (hundreds of rows each): 128x128 GEMM tiles
+    "bf16_fat": Workload("bf16_fat", 11, T=2048, D=128, H=256, d=2, M=4, k=2, dtype="bf16",
+                         act="gelu", p_alive=0.9),
+    # 3-D grid, token count off the tile grid, ReLU
+    "bf16_grid3d": Workload("bf16_grid3d", 12, T=333, D=128, H=192, d=3, M=3, k=4, dtype="bf16",
+                            act="relu", p_alive=0.85),
+    # d = 1 with k = N: a dense softmax mixture
+    "f32_dense": Workload("f32_dense", 13, T=100, D=64, H=128, d=1, M=8, k=8, dtype="f32",
+                          act="gelu"),
+    # skewed gate as in the failure+skew workload, at a small size
+    "bf16_skew": Workload("bf16_skew", 14, T=1024, D=256, H=256, d=2, M=16, k=4, dtype="bf16",
+                          act="gelu", p_alive=0.9, gate_scale=4.0, skew_rows=4),
+    # 4-D grid, fp32
+    "f32_grid4d": Workload("f32_grid4d", 15, T=200, D=64, H=64, d=4, M=3, k=5, dtype="f32",
+                           act="gelu", p_alive=0.7),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_layer_parity(name):
+    wl = CASES[name]
+    say(f"[parity] {name}: T={wl.T} D={wl.D} H={wl.H} d={wl.d} M={wl.M} k={wl.k} {wl.dtype}")
+    inp = make_inputs(wl, "cpu")
+    gpu = gpu_run(wl, inp, backward=wl.backward)
+    fwd, bwd = oracle_run(wl, inp, backward=wl.backward)
+    compare(wl, inp, gpu, fwd, bwd)
+
+
+def test_dh_may_alias_h():
+    wl = CASES["bf16_skinny"]
+    say("[parity] dh aliasing h")
+    inp = make_inputs(wl, "cpu")
+    a = gpu_run(wl, inp, dh_aliases_h=False)
+    b = gpu_run(wl, inp, dh_aliases_h=True)
+    for n in ("dx", "dW1", "dW2", "db1", "db2", "dWg"):
+        assert torch.equal(a[n], b[n]), n
+
+
+def test_all_experts_dead():
+    wl = Workload("dead", 20, T=96, D=64, H=128, d=2, M=4, k=3, dtype="bf16", act="gelu", p_alive=0.0)
+    say("[parity] all experts dead")
+    inp = make_inputs(wl, "cpu")
+    gpu = gpu_run(wl, inp)
+    fwd, bwd = oracle_run(wl, inp)
+    compare(wl, inp, gpu, fwd, bwd)
+    assert int(gpu["offsets"][-1]) == 0
+    assert (gpu["y"].float() == 0).all() and (gpu["w"] == 0).all()
+    assert (gpu["dx"].float() == 0).all() and (gpu["dWg"].float() == 0).all()
+
+
+def test_single_alive_expert():
+    wl = Workload("one_alive", 21, T=128, D=64, H=64, d=2, M=4, k=4, dtype="f32", act="relu")
+    say("[parity] single alive expert")
+    inp = make_inputs(wl, "cpu")
+    alive = torch.zeros(wl.N, dtype=torch.uint8)
+    alive[5] = 1
+    inp["alive"] = alive
+    gpu = gpu_run(wl, inp)
+    fwd, bwd = oracle_run(wl, inp)
+    compare(wl, inp, gpu, fwd, bwd)
+    w = gpu["w"].numpy()
+    chosen = gpu["idx"].numpy() == 5
+    np.testing.assert_array_equal(w[chosen], 1.0)
+    assert (w[~chosen] == 0).all()
+
+
+def test_empty_batch():
+    from paper_2002_04013_amd import DMoELayer
+    say("[parity] T = 0")
+    wl = Workload("empty", 22, T=0, D=64, H=64, d=2, M=4, k=2, dtype="bf16", act="gelu")
+    inp = make_inputs(wl, "cpu")
+    t = {n: v.cuda() for n, v in inp.items()}
+    L = DMoELayer(0, 64, 64, 2, 4, 2, "bf16", "gelu")
+    L.forward(t["x"], t["Wg"], t["bg"], t["alive"], t["W1"], t["b1"], t["W2"], t["b2"])
+    dWg = torch.full_like(t["Wg"], 3.0)
+    dbg = torch.full_like(t["bg"], 3.0)
+    dW1 = torch.full_like(t["W1"], 7.0)
+    L.backward(t["dy"], t["x"], t["Wg"], t["alive"], t["W1"], t["W2"], dW1, t["b1"].clone(),
+               t["W2"].clone(), t["b2"].clone(), dWg, dbg)
+    torch.cuda.synchronize()
+    assert (L.counts.cpu() == 0).all() and (L.offsets.cpu() == 0).all()
+    assert (dWg.float().cpu() == 0).all() and (dbg.float().cpu() == 0).all()
+    assert (dW1.float().cpu() == 7.0).all()
+
+
+def test_identical_experts_invariant():
+    """Every expert equal: y = f(x) for tokens with an alive expert; gate grads 0."""
+    wl = Workload("same", 23, T=256, D=128, H=128, d=2, M=4, k=3, dtype="f32", act="gelu", p_alive=0.75)
+    say("[parity] identical experts")
+    inp = make_inputs(wl, "cpu", identical_experts=True)
+    gpu = gpu_run(wl, inp)
+    import oracle as O
+    f = {n: O.to64(v) for n, v in inp.items()}
+    _, _, y1 = O.expert_forward(f["x"], f["W1"][0], f["b1"][0], f["W2"][0], f["b2"][0], "gelu")
+    live = inp["alive"].numpy()[gpu["idx"].numpy()].astype(bool).any(axis=1)
+    assert_close(gpu["y"].numpy()[live], y1[live], 1e-5, "y vs single expert")
+    assert (gpu["y"].numpy()[~live] == 0).all()
+    np.testing.assert_allclose(gpu["dg"].numpy(), 0, atol=1e-5)
+
+
+def test_deterministic():
+    wl = CASES["bf16_skew"]
+    say("[parity] determinism")
+    inp = make_inputs(wl, "cpu")
+    a = gpu_run(wl, inp)
+    b = gpu_run(wl, inp)
+    for n in a:
+        assert torch.equal(a[n], b[n]) or n in ("row_token", "x_perm", "h", "a", "y_perm", "dy_perm",
+                                                 "dx_perm", "dh"), n
+    rows = int(a["offsets"][-1])
+    for n in ("row_token", "x_perm", "h", "a", "y_perm", "dy_perm", "dx_perm", "dh"):
+        assert torch.equal(a[n][:rows], b[n][:rows]), n
+
+
+def test_token_permutation_equivariance():
+    wl = CASES["bf16_skinny"]
+    say("[parity] token permutation")
+    inp = make_inputs(wl, "cpu")
+    perm = torch.randperm(wl.T, generator=torch.Generator().manual_seed(3))
+    inp2 = dict(inp, x=inp["x"][perm], dy=inp["dy"][perm])
+    a = gpu_run(wl, inp)
+    b = gpu_run(wl, inp2)
+    assert torch.equal(b["idx"], a["idx"][perm])
+    assert torch.equal(b["y"], a["y"][perm])
+    assert torch.equal(b["dx"], a["dx"][perm])

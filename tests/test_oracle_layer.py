@@ -302,3 +302,36 @@ def test_all_dead_tokens_are_zero():
     assert (fwd["y"] == 0).all() and (fwd["w"] == 0).all()
     assert (bwd["dx"] == 0).all() and (bwd["dWg"] == 0).all()
     assert fwd["offsets"][-1] == 0
+
+
+# ------------------------------------------------------------------ bf16 storage rounding
+
+def test_round_bf16_matches_torch_and_ties_to_even():
+    g = torch.Generator().manual_seed(0)
+    v = torch.randn(100000, generator=g) * torch.exp(torch.randn(100000, generator=g) * 5)
+    ref = v.to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(O.round_bf16(v.double().numpy()), ref)
+    # exact halfway cases: 1 + 2^-8 lies between 1 and 1 + 2^-7 -> even (1.0);
+    # 1 + 3*2^-8 lies between 1 + 2^-7 and 1 + 2^-6 -> even (1 + 2^-6)
+    np.testing.assert_array_equal(O.round_bf16(np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -(1 + 2.0 ** -8)])),
+                                  [1.0, 1 + 2.0 ** -6, -1.0])
+    assert O.round_bf16(np.array([0.0]))[0] == 0.0
+
+
+def test_storage_rounding_only_perturbs_at_bf16_level():
+    P = _problem(T=64, D=16, H=24, d=2, M=3, k=3, p=0.8, seed=21)
+    ex = (P["W1"], P["b1"], P["W2"], P["b2"])
+    args = (P["x"], P["Wg"], P["bg"], ex, P["alive"], 2, 3, 3, "gelu")
+    f0 = O.layer_forward(*args)
+    f1 = O.layer_forward(*args, store=O.round_bf16)
+    np.testing.assert_array_equal(f0["idx"], f1["idx"])
+    np.testing.assert_array_equal(f1["h"], O.round_bf16(f0["h"]))
+    np.testing.assert_array_equal(f1["a"], O.round_bf16(f0["a"]))
+    rms = np.sqrt(np.mean(f0["y"] ** 2))
+    assert np.max(np.abs(f1["y"] - f0["y"])) < 2 ** -6 * rms
+    b0 = O.layer_backward(f0, P["dy"], P["x"], P["Wg"], ex, P["alive"], 2, 3, 3, "gelu")
+    b1 = O.layer_backward(f1, P["dy"], P["x"], P["Wg"], ex, P["alive"], 2, 3, 3, "gelu",
+                          store=O.round_bf16)
+    for n in ("dx", "dWg"):
+        rms = np.sqrt(np.mean(b0[n] ** 2))
+        assert np.max(np.abs(b1[n] - b0[n])) < 2 ** -5 * rms, n
