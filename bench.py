@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Benchmark of one DMoE layer, forward + backward, on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload wide]
+
+A step is one pass of the whole layer over one batch of synthetic input:
+gate + TopK + weights, dispatch, expert FFN forward, combine, and the backward of
+all of them (combine, gate, expert FFN, dispatch).  Inputs and weights are
+resident in HBM before the timed region.  Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "DMoE layer fwd+bwd tokens/sec on 1 MI355X; expert-GEMM MFMA util %; gate HBM GB/s"
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+CALLS = ("gate_topk", "dispatch", "ffn_fwd", "combine", "combine_bwd", "gate_topk_bwd", "ffn_bwd",
+         "dispatch_bwd")
+
+
+def algorithmic(wl, counts):
+    """Algorithmic bytes and flops per call (what the method must move/compute)."""
+    e = 2 if wl.dtype == "bf16" else 4
+    T, D, H, dM, k = wl.T, wl.D, wl.H, wl.dM, wl.k
+    rows = int(sum(counts))
+    touched = int(sum(1 for c in counts if c > 0))
+    wbytes = touched * (2 * D * H + H + D) * e
+    out = {}
+    out["gate_topk"] = dict(bytes=T * D * e + dM * D * e + T * k * 12, flops=2 * T * D * dM)
+    out["dispatch"] = dict(bytes=T * D * e + rows * D * e + T * k * 12, flops=0)
+    out["ffn_fwd"] = dict(bytes=wbytes + rows * (D * e + 3 * H * e + D * e), flops=4 * rows * D * H)
+    out["combine"] = dict(bytes=rows * D * e + T * D * e, flops=2 * rows * D)
+    out["combine_bwd"] = dict(bytes=T * D * e + 2 * rows * D * e, flops=4 * rows * D)
+    out["gate_topk_bwd"] = dict(bytes=T * D * e + dM * D * e, flops=2 * T * D * dM)
+    # dh: read dy_perm, W2, h; write dh.  dW2: read dy_perm, a; write dW2.
+    # dx_perm: read dh, W1; write dx_perm.  dW1: read dh, x_perm; write dW1.
+    out["ffn_bwd"] = dict(bytes=2 * wbytes + rows * (D * e + 2 * H * e) + rows * (D * e + H * e)
+                          + rows * (H * e + D * e) + rows * (H * e + D * e), flops=8 * rows * D * H)
+    out["dispatch_bwd"] = dict(bytes=rows * D * e + T * D * e + T * k * dM * 0, flops=0)
+    return out
+
+
+def cpu_baseline(wl, inp, counts, budget_s=12.0):
+    """The oracle, as it stands, on a bounded sample of the same workload: routing
+    (gate, TopK, weights), dispatch and the gate backward for every token, then the
+    expert blocks forward+backward for a few experts, extrapolated linearly in pairs
+    to the whole batch."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
+                      or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    x = O.to64(inp["x"])
+    Wg, bg = O.to64(inp["Wg"]), O.to64(inp["bg"])
+    alive = inp["alive"].cpu().numpy()
+    dy = O.to64(inp["dy"])
+    N = wl.N
+
+    t0 = time.perf_counter()
+    r = O.routing(x, Wg, bg, alive, wl.d, wl.M, wl.k)
+    c, off, row_token, pos = O.dispatch(r["idx"], alive, N)
+    O.gate_backward(r["w"], np.zeros_like(r["w"]), r["idx"], alive, x, Wg, wl.d, wl.M)
+    t_route = time.perf_counter() - t0
+
+    live = [int(e) for e in np.nonzero(c)[0]]
+    rng = np.random.default_rng(0)
+    rng.shuffle(live)
+    t_exp, pairs, used = 0.0, 0, 0
+    for e in live:
+        W1, b1, W2, b2 = (O.to64(inp[n][e]) for n in ("W1", "b1", "W2", "b2"))   # not timed
+        rows = row_token[off[e]:off[e + 1]]
+        t1 = time.perf_counter()
+        X = x[rows]
+        h, a, y = O.expert_forward(X, W1, b1, W2, b2, wl.act)
+        O.expert_backward(X, h, a, dy[rows], W1, W2, wl.act)
+        t_exp += time.perf_counter() - t1
+        pairs += len(rows)
+        used += 1
+        if t_exp + t_route > budget_s or used >= 16:
+            break
+    total_pairs = int(off[-1])
+    est = t_route + t_exp * total_pairs / max(pairs, 1)
+    return {"value": round(wl.T / est, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle: routing, dispatch and gate backward for all {wl.T} tokens "
+                       f"({t_route:.2f} s) + expert fwd+bwd for {used} experts ({pairs} of "
+                       f"{total_pairs} pairs, {t_exp:.2f} s), extrapolated linearly in pairs"),
+            "seconds_measured": round(t_route + t_exp, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="wide")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    ws_env = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or ws_env != 1:
+        print("bench.py: this build runs the DMoE layer on one GPU only; "
+              "multi-GPU (--gpus > 1) is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2002_04013_amd import DMoELayer
+    from workloads import get_workload, make_alive, make_dy, make_experts, make_gate, make_x
+
+    wl = get_workload(args.workload)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.perf_counter()
+    Wg, bg = make_gate(wl, dev)
+    inp = dict(x=make_x(wl, dev), dy=make_dy(wl, dev), Wg=Wg, bg=bg, alive=make_alive(wl, dev))
+    W1, b1, W2, b2 = make_experts(wl, dev)
+    inp.update(W1=W1, b1=b1, W2=W2, b2=b2)
+    dW1, db1 = torch.empty_like(W1), torch.empty_like(b1)
+    dW2, db2 = torch.empty_like(W2), torch.empty_like(b2)
+    dWg, dbg = torch.empty_like(Wg), torch.empty_like(bg)
+    L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, dh_aliases_h=False)
+    torch.cuda.synchronize()
+    print(f"[bench] {wl.name}: inputs ready in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr,
+          flush=True)
+
+    x, alive = inp["x"], inp["alive"]
+    from paper_2002_04013_amd import abi
+    Dm = L.dims
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        calls = [
+            ("gate_topk", lambda: abi.dmoe_gate_topk(Dm, x, Wg, bg, alive, L.idx, L.w, None, None, L.ws)),
+            ("dispatch", lambda: abi.dmoe_dispatch(Dm, x, L.idx, alive, L.counts, L.offsets, L.row_token,
+                                                   L.pos, L.x_perm, L.ws)),
+            ("ffn_fwd", lambda: abi.dmoe_expert_ffn_fwd(Dm, L.offsets, L.x_perm, W1, b1, W2, b2, L.h, L.a,
+                                                        L.y_perm, L.ws)),
+            ("combine", lambda: abi.dmoe_combine(Dm, L.y_perm, L.pos, L.w, L.y)),
+            ("combine_bwd", lambda: abi.dmoe_combine_bwd(Dm, inp["dy"], L.y_perm, L.pos, L.w, L.dy_perm,
+                                                         L.dw)),
+            ("gate_topk_bwd", lambda: abi.dmoe_gate_topk_bwd(Dm, x, L.idx, L.w, L.dw, alive, L.dg, dWg, dbg,
+                                                             L.ws)),
+            ("ffn_bwd", lambda: abi.dmoe_expert_ffn_bwd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
+                                                        L.dy_perm, W1, W2, L.dh, L.dx_perm, dW1, db1, dW2,
+                                                        db2, L.ws)),
+            ("dispatch_bwd", lambda: abi.dmoe_dispatch_bwd(Dm, L.dx_perm, L.pos, L.idx, L.dg, Wg, L.dx)),
+        ]
+        for name, fn in calls:
+            if ev is not None:
+                ev[name][0].record(stream)
+            fn()
+            if ev is not None:
+                ev[name][1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    counts = L.counts.cpu().tolist()
+
+    evs = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in CALLS}
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in evs) / args.steps for n in CALLS}
+    print(f"[bench] {args.steps} steps in {wall:.3f} s; per call ms: " +
+          ", ".join(f"{n} {v:.3f}" for n, v in ms.items()), file=sys.stderr, flush=True)
+
+    alg = algorithmic(wl, counts)
+    peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    ridge = peak_tf * 1e12 / (PEAK_HBM_GBS * 1e9)
+
+    def roof(name):
+        a = alg[name]
+        t = ms[name] * 1e-3
+        ai = a["flops"] / max(a["bytes"], 1)
+        if a["flops"] and ai >= ridge:
+            ach = a["flops"] / t / 1e12
+            return {"bound": "mfma", "achieved": round(ach, 1), "peak": peak_tf, "unit": "TFLOP/s",
+                    "frac": round(ach / peak_tf, 4)}
+        ach = a["bytes"] / t / 1e9
+        return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4)}
+
+    roofline = dict(roof("ffn_fwd"), kernel="grouped_gemm (dmoe_expert_ffn_fwd: up- and down-projection "
+                    "launches + 1-block tile plan)", traffic=None,
+                    per_launch={"flops": alg["ffn_fwd"]["flops"], "bytes": alg["ffn_fwd"]["bytes"],
+                                "ms": round(ms["ffn_fwd"], 4)})
+    result = {
+        "metric": METRIC,
+        "value": round(wl.T * args.steps / wall, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded N(0,1) inputs, N(0,1/fan_in) weights, random init)",
+        "config": {"workload": wl.name, "tokens": wl.T, "d_model": wl.D, "expert_hidden": wl.H,
+                   "grid": f"{'x'.join([str(wl.M)] * wl.d)}", "experts": wl.N, "k": wl.k,
+                   "act": wl.act, "p_alive": wl.p_alive, "pass": "fwd+bwd"},
+        "roofline": roofline,
+        "roofline_ffn_bwd": roof("ffn_bwd"),
+        "gate_topk": roof("gate_topk"),
+        "dispatch": roof("dispatch"),
+        "calls_ms": {n: round(v, 4) for n, v in ms.items()},
+    }
+    if not args.no_cpu_baseline:
+        host = {n: v for n, v in inp.items()}
+        for n in ("x", "dy", "Wg", "bg", "alive"):
+            host[n] = inp[n].cpu()
+        result["cpu_baseline"] = cpu_baseline(wl, host, counts)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

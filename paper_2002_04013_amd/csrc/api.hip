@@ -44,7 +44,7 @@ Workspace workspace_layout(const Shape& s) {
   w.gsplit_tokens = split;
   w.gsplit = s.T > 0 ? (s.T + split - 1) / split : 0;
   // tile bookkeeping: GEMM tile prefix [N+1] (+ split offsets/prefix of the gate GEMM)
-  const int64_t tiles_ints = (s.N + 1) + 2 * (w.gsplit + 1);
+  const int64_t tiles_ints = 2 * (s.N + 1) + 2 * (w.gsplit + 1);
   w.tiles_off = off;
   w.tiles_bytes = align256((size_t)tiles_ints * sizeof(int32_t));
   off += w.tiles_bytes;

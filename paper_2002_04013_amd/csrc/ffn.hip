@@ -7,34 +7,45 @@
 
 namespace dmoe {
 
-// tprefix[e] = tiles of experts before e:
-//   GROUP_M: ceil(rows_e / BM) * tiles_per;   GROUP_K: tiles_per if rows_e > 0.
+// Tile plan of one FFN call, from the expert row offsets:
+//   plan[e]         = sum over experts before e of ceil(rows / BM)   (GROUP_M m-tiles)
+//   plan[N + 1 + e] = number of experts before e that have rows      (GROUP_K experts)
+// A GEMM with NT n-tiles (GROUP_M) or MT*NT tiles per expert (GROUP_K) scales these.
 __global__ void __launch_bounds__(1024)
-tile_prep(const int32_t* offsets, int N, int mode, int BM, int tiles_per, int32_t* tprefix) {
-  __shared__ int sums[1024];
+tile_plan(const int32_t* offsets, int N, int BM, int32_t* plan) {
+  __shared__ int s_mt[1024], s_ac[1024];
   const int q = threadIdx.x;
   const int EPT = (N + 1023) / 1024;
   const int e0 = min(N, q * EPT), e1 = min(N, e0 + EPT);
-  int mine = 0;
+  int mt = 0, ac = 0;
   for (int e = e0; e < e1; ++e) {
     const int c = offsets[e + 1] - offsets[e];
-    mine += mode == GROUP_M ? (c + BM - 1) / BM * tiles_per : (c > 0 ? tiles_per : 0);
+    mt += (c + BM - 1) / BM;
+    ac += c > 0;
   }
-  sums[q] = mine;
+  s_mt[q] = mt;
+  s_ac[q] = ac;
   __syncthreads();
   for (int o = 1; o < 1024; o <<= 1) {
-    const int v = q >= o ? sums[q - o] : 0;
+    const int a = q >= o ? s_mt[q - o] : 0, b = q >= o ? s_ac[q - o] : 0;
     __syncthreads();
-    sums[q] += v;
+    s_mt[q] += a;
+    s_ac[q] += b;
     __syncthreads();
   }
-  int base = sums[q] - mine;
+  int bm = s_mt[q] - mt, ba = s_ac[q] - ac;
+  int32_t* act = plan + N + 1;
   for (int e = e0; e < e1; ++e) {
-    tprefix[e] = base;
+    plan[e] = bm;
+    act[e] = ba;
     const int c = offsets[e + 1] - offsets[e];
-    base += mode == GROUP_M ? (c + BM - 1) / BM * tiles_per : (c > 0 ? tiles_per : 0);
+    bm += (c + BM - 1) / BM;
+    ba += c > 0;
   }
-  if (q == 1023) tprefix[N] = sums[1023];
+  if (q == 1023) {
+    plan[N] = s_mt[1023];
+    act[N] = s_ac[1023];
+  }
 }
 
 // out[e][c] = sum of rows [offsets[e], offsets[e+1]) of X[:, c]  (bias gradients);
@@ -92,9 +103,9 @@ static void run_gemm(GemmArgs<E> p, int64_t tiles_ub, hipStream_t st) {
 }
 
 template <typename E>
-static GemmArgs<E> args_m(const int32_t* offsets, const int32_t* tpre, int N) {
+static GemmArgs<E> args_m(const int32_t* offsets, const int32_t* tpre, int scale, int N) {
   GemmArgs<E> p{};
-  p.offsets = offsets; p.tprefix = tpre; p.groups = N;
+  p.offsets = offsets; p.tprefix = tpre; p.tscale = scale; p.groups = N;
   return p;
 }
 
@@ -112,11 +123,11 @@ static void ffn_fwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
                         hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   // h = x W1^T + b1, a = act(h)
   {
     const int nt = (H + C::BN - 1) / C::BN;
-    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_M, C::BM, nt, tpre);
-    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, nt, N);
     p.A = xp; p.lda = D;
     p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
     p.C = h; p.ldc = H; p.C2 = a;
@@ -127,8 +138,7 @@ static void ffn_fwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   // y = a W2^T + b2
   {
     const int nt = (D + C::BN - 1) / C::BN;
-    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_M, C::BM, nt, tpre);
-    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, nt, N);
     p.A = a; p.lda = H;
     p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
     p.C = yp; p.ldc = D;
@@ -145,11 +155,12 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
   const int64_t active_ub = std::min<int64_t>(s.N, s.P);
+  const int32_t* tact = tpre + N + 1;
+  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   // dh = (dy W2) * act'(h)       B = W2_e viewed as (n = h, k = d): N-contiguous
   {
     const int nt = (H + C::BN - 1) / C::BN;
-    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_M, C::BM, nt, tpre);
-    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, nt, N);
     p.A = dyp; p.lda = D;
     p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
     p.C = dh; p.ldc = H; p.aux = h;
@@ -159,8 +170,7 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   // dW2_e = dy_e^T a_e   [D, H]
   {
     const int mt = (D + CW::BM - 1) / CW::BM, nt = (H + CW::BN - 1) / CW::BN;
-    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_K, 0, mt * nt, tpre);
-    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    GemmArgs<E> p = args_m<E>(offsets, tact, mt * nt, N);
     p.A = dyp; p.lda = D;
     p.B = a; p.ldb = H;
     p.C = dW2; p.ldc = H; p.c_gstride = (int64_t)D * H;
@@ -170,8 +180,7 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   // dx_perm = dh W1              B = W1_e viewed as (n = d, k = h): N-contiguous
   {
     const int nt = (D + C::BN - 1) / C::BN;
-    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_M, C::BM, nt, tpre);
-    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    GemmArgs<E> p = args_m<E>(offsets, tpre, nt, N);
     p.A = dh; p.lda = H;
     p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
     p.C = dxp; p.ldc = D;
@@ -181,8 +190,7 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   // dW1_e = dh_e^T x_e   [H, D]
   {
     const int mt = (H + CW::BM - 1) / CW::BM, nt = (D + CW::BN - 1) / CW::BN;
-    hipLaunchKernelGGL(tile_prep, dim3(1), dim3(1024), 0, st, offsets, N, (int)GROUP_K, 0, mt * nt, tpre);
-    GemmArgs<E> p = args_m<E>(offsets, tpre, N);
+    GemmArgs<E> p = args_m<E>(offsets, tact, mt * nt, N);
     p.A = dh; p.lda = H;
     p.B = xp; p.ldb = D;
     p.C = dW1; p.ldc = D; p.c_gstride = (int64_t)H * D;

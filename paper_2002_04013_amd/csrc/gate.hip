@@ -246,12 +246,11 @@ __global__ void gate_dg_kernel(const int32_t* idx, const float* w, const float* 
 }
 
 // offsets of the token splits and the GROUP_K tile prefix for the dWg GEMM
-__global__ void gate_split_prep(int32_t* offs, int32_t* tprefix, int nsplit, int split, int T,
-                                int tiles_per_split) {
+__global__ void gate_split_prep(int32_t* offs, int32_t* tprefix, int nsplit, int split, int T) {
   for (int s = threadIdx.x; s <= nsplit; s += blockDim.x) {
     const int o = s * split;
     offs[s] = o < T ? o : T;
-    tprefix[s] = s * tiles_per_split;
+    tprefix[s] = s;
   }
 }
 
@@ -334,12 +333,12 @@ static int gate_bwd_impl(const Shape& s, const void* x, const int32_t* idx, cons
   const int rows = (int)L.ds_ld;                     // GEMM M (ds columns incl. lo part/padding)
   const int mt = (rows + BM - 1) / BM, nt = (D + BN - 1) / BN;
   hipLaunchKernelGGL(gate_split_prep, dim3(1), dim3(256), 0, st, offs, tpre, (int)L.gsplit,
-                     (int)L.gsplit_tokens, T, mt * nt);
+                     (int)L.gsplit_tokens, T);
   GemmArgs<E> p{};
   p.A = ds; p.lda = L.ds_ld;
   p.B = reinterpret_cast<const E*>(x); p.ldb = D;
   p.C = part; p.ldc = D; p.c_gstride = (int64_t)rows * D;
-  p.offsets = offs; p.tprefix = tpre; p.groups = (int)L.gsplit;
+  p.offsets = offs; p.tprefix = tpre; p.tscale = mt * nt; p.groups = (int)L.gsplit;
   p.M = rows; p.N = D; p.K = 0; p.act = s.act;
   const int tiles = (int)L.gsplit * mt * nt;
   auto kern = grouped_gemm<E, GROUP_K, false, EPI_F32, BM, BN, BK, WM, WN>;

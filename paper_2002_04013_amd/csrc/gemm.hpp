@@ -46,7 +46,8 @@ struct GemmArgs {
   const E* bias; int64_t bias_gstride;             // EPI_BIAS*: per-expert bias [N]
   const E* aux;                                    // EPI_DACT: pre-activation, layout of C
   const int32_t* offsets;                          // [groups+1]
-  const int32_t* tprefix;                          // [groups+1] tile prefix (tile_prep)
+  const int32_t* tprefix;                          // [groups+1] prefix of tile units
+  int tscale;                                      // tiles per unit of tprefix
   int groups;
   int M, N, K;                                     // fixed dims (M unused for GROUP_M, K for GROUP_K)
   int act;
@@ -145,12 +146,13 @@ struct TileT {
   }
 };
 
-// Tile lookup: expert e owning global tile L (tprefix is non-decreasing).
-__device__ __forceinline__ int find_group(const int32_t* tprefix, int groups, int L) {
-  int lo = 0, hi = groups;          // invariant: tprefix[lo] <= L < tprefix[hi]
+// Tile lookup: expert e owning global tile L; expert e's tiles start at
+// tprefix[e] * scale (tprefix is non-decreasing).
+__device__ __forceinline__ int find_group(const int32_t* tprefix, int scale, int groups, int L) {
+  int lo = 0, hi = groups;          // invariant: tprefix[lo]*scale <= L < tprefix[hi]*scale
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
-    if (tprefix[mid] <= L) lo = mid; else hi = mid;
+    if (tprefix[mid] * scale <= L) lo = mid; else hi = mid;
   }
   return lo;
 }
@@ -176,7 +178,7 @@ grouped_gemm(GemmArgs<E> p) {
   const int wm = wave % WM, wn = wave / WM;
   const int l32 = lane & 31, lhi = lane >> 5;
 
-  const int total = p.tprefix[p.groups];
+  const int total = p.tprefix[p.groups] * p.tscale;
   const int nblk = gridDim.x;
   int L, Lend, Lstep;
   if (p.chunked) {
@@ -193,8 +195,8 @@ grouped_gemm(GemmArgs<E> p) {
   const int NTILES = (p.N + BN - 1) / BN;
 
   for (; L < Lend; L += Lstep) {
-    const int e = find_group(p.tprefix, p.groups, L);
-    const int q = L - p.tprefix[e];
+    const int e = find_group(p.tprefix, p.tscale, p.groups, L);
+    const int q = L - p.tprefix[e] * p.tscale;
     const int off = p.offsets[e];
     const int cnt = p.offsets[e + 1] - off;
     int m0, n0, mvalid, kvalid;
