@@ -4,6 +4,7 @@
 
 #include "common.hpp"
 #include "gemm.hpp"
+#include "gemm2.hpp"
 
 namespace dmoe {
 
@@ -102,6 +103,27 @@ static void run_gemm(GemmArgs<E> p, int64_t tiles_ub, hipStream_t st) {
   hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
 }
 
+// gfx950 bf16 path: direct-to-LDS multi-stage GEMM (gemm2.hpp)
+template <int GM, bool AT, bool BT, int EPI, int BM, int BN, int WM, int WN, int ST>
+static void run_gemm2(GemmArgs<bf16> p, int64_t tiles_ub, hipStream_t st) {
+  if (tiles_ub <= 0) return;
+  auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1>;
+  constexpr int NT = 64 * WM * WN;
+  const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT>();
+  static int per_cu = 0;
+  if (!per_cu) {
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, NT, lds) != hipSuccess || nb < 1) nb = 1;
+    (void)hipGetLastError();
+    per_cu = nb;
+  }
+  const int64_t resident = (int64_t)per_cu * device_cus();
+  const int grid = (int)std::min<int64_t>(tiles_ub, resident);
+  p.chunked = grid >= 8;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
+}
+
 template <typename E>
 static GemmArgs<E> args_m(const int32_t* offsets, const int32_t* tpre, int scale, int N) {
   GemmArgs<E> p{};
@@ -109,13 +131,95 @@ static GemmArgs<E> args_m(const int32_t* offsets, const int32_t* tpre, int scale
   return p;
 }
 
-// Tile shapes.  bf16: few rows per expert -> 32-row tiles that stream the weights
-// (256 weight rows per tile); many rows -> 128x128 tiles.  fp32: small tiles.
-struct CfgSkinny { static constexpr int BM = 32, BN = 256, BK = 32, WM = 1, WN = 4; };
-struct CfgFat    { static constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2; };
+// fp32 tile shapes (register-staged MFMA GEMM of gemm.hpp).
 struct CfgF32    { static constexpr int BM = 32, BN = 64, BK = 32, WM = 1, WN = 2; };
-struct CfgDW     { static constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2; };
 struct CfgDWF32  { static constexpr int BM = 64, BN = 64, BK = 32, WM = 2, WN = 2; };
+
+// bf16 tile shapes of the gemm2 path: many rows per expert -> 256x256 tiles, 8 waves,
+// 2 stages (MFMA-bound); few rows -> 32x256 tiles, 4 waves, 4 stages (weight streaming).
+struct G2Fat    { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2; };
+struct G2Skinny { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4; };
+struct G2DW     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2; };
+
+template <typename C>
+static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, const bf16* W1,
+                         const bf16* b1, const bf16* W2, const bf16* b2, bf16* h, bf16* a, bf16* yp,
+                         int32_t* tpre, hipStream_t st) {
+  const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
+  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  {
+    const int nt = (H + C::BN - 1) / C::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
+    p.A = xp; p.lda = D;
+    p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
+    p.C = h; p.ldc = H; p.C2 = a;
+    p.bias = b1; p.bias_gstride = H;
+    p.N = H; p.K = D; p.act = s.act;
+    run_gemm2<GROUP_M, false, false, EPI_BIAS_ACT, C::BM, C::BN, C::WM, C::WN, C::ST>(p, mt_ub * nt, st);
+  }
+  {
+    const int nt = (D + C::BN - 1) / C::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
+    p.A = a; p.lda = H;
+    p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
+    p.C = yp; p.ldc = D;
+    p.bias = b2; p.bias_gstride = D;
+    p.N = D; p.K = H; p.act = s.act;
+    run_gemm2<GROUP_M, false, false, EPI_BIAS, C::BM, C::BN, C::WM, C::WN, C::ST>(p, mt_ub * nt, st);
+  }
+}
+
+template <typename C, typename CW>
+static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, const bf16* h,
+                         const bf16* a, const bf16* dyp, const bf16* W1, const bf16* W2, bf16* dh, bf16* dxp,
+                         bf16* dW1, bf16* db1, bf16* dW2, bf16* db2, int32_t* tpre, hipStream_t st) {
+  const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
+  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  const int64_t active_ub = std::min<int64_t>(s.N, s.P);
+  const int32_t* tact = tpre + N + 1;
+  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  {   // dh = (dy W2) * act'(h): W2_e read as (n = h, k = d), N-contiguous
+    const int nt = (H + C::BN - 1) / C::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
+    p.A = dyp; p.lda = D;
+    p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
+    p.C = dh; p.ldc = H; p.aux = h;
+    p.N = H; p.K = D; p.act = s.act;
+    run_gemm2<GROUP_M, false, true, EPI_DACT, C::BM, C::BN, C::WM, C::WN, C::ST>(p, mt_ub * nt, st);
+  }
+  {   // dW2_e = dy_e^T a_e   [D, H]
+    const int mt = (D + CW::BM - 1) / CW::BM, nt = (H + CW::BN - 1) / CW::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tact, mt * nt, N);
+    p.A = dyp; p.lda = D;
+    p.B = a; p.ldb = H;
+    p.C = dW2; p.ldc = H; p.c_gstride = (int64_t)D * H;
+    p.M = D; p.N = H; p.act = s.act;
+    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST>(p, active_ub * mt * nt, st);
+  }
+  {   // dx_perm = dh W1: W1_e read as (n = d, k = h), N-contiguous
+    const int nt = (D + C::BN - 1) / C::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
+    p.A = dh; p.lda = H;
+    p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
+    p.C = dxp; p.ldc = D;
+    p.N = D; p.K = H; p.act = s.act;
+    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST>(p, mt_ub * nt, st);
+  }
+  {   // dW1_e = dh_e^T x_e   [H, D]
+    const int mt = (H + CW::BM - 1) / CW::BM, nt = (D + CW::BN - 1) / CW::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tact, mt * nt, N);
+    p.A = dh; p.lda = H;
+    p.B = xp; p.ldb = D;
+    p.C = dW1; p.ldc = D; p.c_gstride = (int64_t)H * D;
+    p.M = H; p.N = D; p.act = s.act;
+    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST>(p, active_ub * mt * nt, st);
+  }
+  hipLaunchKernelGGL(segment_colsum<bf16>, dim3((unsigned)((H / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
+                     st, dh, (int64_t)H, offsets, H, db1);
+  hipLaunchKernelGGL(segment_colsum<bf16>, dim3((unsigned)((D / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
+                     st, dyp, (int64_t)D, offsets, D, db2);
+}
 
 template <typename E, typename C>
 static void ffn_fwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, const E* W1,
@@ -228,9 +332,9 @@ extern "C" int dmoe_expert_ffn_fwd(const dmoe_dims* dims, const int32_t* offsets
     auto c = [](const void* q) { return reinterpret_cast<const bf16*>(q); };
     auto m = [](void* q) { return reinterpret_cast<bf16*>(q); };
     if (use_fat(s))
-      ffn_fwd_cfg<bf16, CfgFat>(s, offsets, c(x_perm), c(W1), c(b1), c(W2), c(b2), m(h), m(a), m(y_perm), tpre, st);
+      ffn_fwd_bf16<G2Fat>(s, offsets, c(x_perm), c(W1), c(b1), c(W2), c(b2), m(h), m(a), m(y_perm), tpre, st);
     else
-      ffn_fwd_cfg<bf16, CfgSkinny>(s, offsets, c(x_perm), c(W1), c(b1), c(W2), c(b2), m(h), m(a), m(y_perm), tpre, st);
+      ffn_fwd_bf16<G2Skinny>(s, offsets, c(x_perm), c(W1), c(b1), c(W2), c(b2), m(h), m(a), m(y_perm), tpre, st);
   } else {
     auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };
     auto m = [](void* q) { return reinterpret_cast<float*>(q); };
@@ -261,11 +365,11 @@ extern "C" int dmoe_expert_ffn_bwd(const dmoe_dims* dims, const int32_t* offsets
     auto c = [](const void* q) { return reinterpret_cast<const bf16*>(q); };
     auto m = [](void* q) { return reinterpret_cast<bf16*>(q); };
     if (use_fat(s))
-      ffn_bwd_cfg<bf16, CfgFat, CfgDW>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
-                                       m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
+      ffn_bwd_bf16<G2Fat, G2DW>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
+                                m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
     else
-      ffn_bwd_cfg<bf16, CfgSkinny, CfgDW>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
-                                          m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
+      ffn_bwd_bf16<G2Skinny, G2DW>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
+                                   m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
   } else {
     auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };
     auto m = [](void* q) { return reinterpret_cast<float*>(q); };

@@ -1,0 +1,313 @@
+// Grouped bf16 GEMM, second design: direct global->LDS loads (16 bytes per lane,
+// no staging registers) into a ring of STAGES LDS buffers, XOR-swizzled tile
+// layouts, and MFMA operand fragments read with ds_read_b128 (K-contiguous
+// tiles) or with the transposing ds_read_b64_tr_b16 (N-contiguous tiles).
+//
+// Same problem statement and tile schedule as grouped_gemm in gemm.hpp:
+//   C[m][n] = sum_k A[m][k] B[n][k] per expert; GROUP_M groups rows (tokens),
+//   GROUP_K groups the contraction (tokens) for weight gradients.
+// Operand storage:
+//   A_T = false: A[m][k] at A[m*lda + k]        A_T = true: A[m][k] at A[k*lda + m]
+//   B_T = false: B[n][k] at B[n*ldb + k]        B_T = true: B[n][k] at B[k*ldb + n]
+//
+// LDS tile layouts (bf16, 16-byte chunks):
+//   K-contiguous tile [R][BK=64]: row r holds 8 chunks; chunk c of row r is stored
+//     at position c ^ swz(r).  A wave's load instruction fills 8 whole rows.
+//   N-contiguous tile [BK][R]: row k holds R/8 chunks; chunk c of row k is stored
+//     at position c ^ (4 * (k % 4)) (R >= 128).  An instruction fills 1024/(2R) rows.
+// Rows beyond the valid m/n range are loaded from a clamped address (their output
+// is never stored); k rows beyond the valid range (GROUP_K tail) are zeroed in LDS.
+#pragma once
+
+#include "gemm.hpp"
+
+namespace dmoe {
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* glb_ptr_t;
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void g2l_16(const void* g, void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((glb_ptr_t)g, (lds_ptr_t)lds_wave_base, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) with expcnt/lgkmcnt left free (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier without a memory fence: orders this wave's LDS accesses
+// (lgkmcnt) but leaves global loads in flight; LDS data written by the direct
+// loads is covered by the explicit vmcnt waits before it.
+__device__ __forceinline__ void block_sync_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int SW>
+__device__ __forceinline__ int swz_kc(int r) { return SW == 0 ? (r & 7) : ((r >> 1) & 7); }
+
+// ---- K-contiguous tile [R][64] -------------------------------------------------------
+template <int R, int NW, int SW>
+struct KcTile {
+  static constexpr int BYTES = R * 128;
+  static constexpr int INSTR = R / 8;                  // 1 KB wave instructions per tile
+  static constexpr int PER_WAVE = (INSTR + NW - 1) / NW;
+  static_assert(R % 8 == 0, "rows");
+  // issue this wave's loads: rows [0, R) of the tile starting at `base` (row stride ld)
+  __device__ __forceinline__ static void load(const bf16* base, int64_t ld, int rvalid, char* lds, int wave,
+                                              int lane) {
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int q = wave + i * NW;
+      if (INSTR % NW != 0 && q >= INSTR) break;
+      const int r = q * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ swz_kc<SW>(r);
+      const int rr = r < rvalid ? r : rvalid - 1;
+      g2l_16(base + (int64_t)rr * ld + c * 8, lds + q * 1024);
+    }
+  }
+  // fragment of rows r0 + (lane % 32), k chunk kc + lane / 32 (8 bf16)
+  __device__ __forceinline__ static bf16x8_t frag(const char* lds, int r0, int kc, int lane) {
+    const int r = r0 + (lane & 31);
+    const int c = (kc + (lane >> 5)) ^ swz_kc<SW>(r);
+    return *reinterpret_cast<const bf16x8_t*>(lds + r * 128 + c * 16);
+  }
+};
+
+// ---- N-contiguous tile [64][R] (row = k) ---------------------------------------------
+template <int R, int NW>
+struct NcTile {
+  static constexpr int BYTES = 64 * R * 2;
+  static constexpr int CPR = R / 8;                    // chunks per row
+  static constexpr int RPI = 1024 / (R * 2);           // rows per wave instruction
+  static constexpr int INSTR = 64 / RPI;
+  static constexpr int PER_WAVE = (INSTR + NW - 1) / NW;
+  static_assert(R >= 128 && R <= 512 && (R & (R - 1)) == 0, "cols");
+  __device__ __forceinline__ static int swz(int k) { return 4 * (k & 3); }
+  // element (col c, k) at base[k * ld + c]; rows k >= kvalid clamped (zeroed later)
+  __device__ __forceinline__ static void load(const bf16* base, int64_t ld, int cvalid, int kvalid, char* lds,
+                                              int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int q = wave + i * NW;
+      if (INSTR % NW != 0 && q >= INSTR) break;
+      const int k = q * RPI + lane / CPR;
+      const int pos = lane % CPR;
+      const int c = pos ^ swz(k);
+      int col = c * 8;
+      col = col < cvalid ? col : ((cvalid - 1) & ~7);
+      const int kk = k < kvalid ? k : kvalid - 1;
+      g2l_16(base + (int64_t)kk * ld + col, lds + q * 1024);
+    }
+  }
+  // zero rows [kvalid, 64) of the tile (GROUP_K tail)
+  __device__ __forceinline__ static void zero_tail(char* lds, int kvalid, int tid, int nt) {
+    uint4* p = reinterpret_cast<uint4*>(lds + kvalid * R * 2);
+    const int n = (64 - kvalid) * CPR;
+    for (int i = tid; i < n; i += nt) p[i] = make_uint4(0, 0, 0, 0);
+  }
+  // MFMA fragment for columns c0 .. c0+31 (lane % 32) and k = kk .. kk+15 (lane / 32 picks 8):
+  // two transposing reads, 4 k each.
+  __device__ __forceinline__ static bf16x8_t frag(const char* lds, int c0, int kk, int lane) {
+    const int g = lane >> 4, i = lane & 15;
+    const int col = c0 + 16 * (g & 1) + 4 * (i & 3);
+    const int chunk = col >> 3, within = (col & 7) * 2;
+    s16x4_t lo, hi;
+    {
+      const int k = kk + 8 * (g >> 1) + (i >> 2);
+      const char* a = lds + k * (R * 2) + ((chunk ^ swz(k)) << 4) + within;
+      lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(a));
+    }
+    {
+      const int k = kk + 8 * (g >> 1) + 4 + (i >> 2);
+      const char* a = lds + k * (R * 2) + ((chunk ^ swz(k)) << 4) + within;
+      hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(a));
+    }
+    typedef short s16x8_t __attribute__((ext_vector_type(8)));
+    s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8_t, v);
+  }
+};
+
+template <int GM, bool A_T, bool B_T, int EPI, int BM, int BN, int WM, int WN, int STAGES, int SW>
+__global__ void __launch_bounds__(64 * WM * WN)
+grouped_gemm2(GemmArgs<bf16> p) {
+  constexpr int NW = WM * WN, NT = 64 * NW, BK = 64;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  using TA = typename std::conditional<A_T, NcTile<BM, NW>, KcTile<BM, NW, SW>>::type;
+  using TB = typename std::conditional<B_T, NcTile<BN, NW>, KcTile<BN, NW, SW>>::type;
+  constexpr int ABYTES = TA::BYTES, SBYTES = TA::BYTES + TB::BYTES;
+  static_assert(TM >= 1 && TN >= 1, "tile");
+  static_assert(TA::INSTR % NW == 0 && TB::INSTR % NW == 0, "equal load counts per wave");
+  static_assert(GM == GROUP_M || (A_T && B_T), "GROUP_K takes both operands stored per token");
+
+  extern __shared__ __align__(1024) char smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave % WM, wn = wave / WM;
+
+  const int total = p.tprefix[p.groups] * p.tscale;
+  int L, Lend, Lstep;
+  if (p.chunked) {
+    const int x = blockIdx.x & 7, lb = blockIdx.x >> 3;
+    L = (int)(((int64_t)x * total) >> 3) + lb;
+    Lend = (int)(((int64_t)(x + 1) * total) >> 3);
+    Lstep = (gridDim.x - x + 7) >> 3;
+  } else {
+    L = blockIdx.x; Lend = total; Lstep = gridDim.x;
+  }
+  const int NTILES = (p.N + BN - 1) / BN;
+
+  for (; L < Lend; L += Lstep) {
+    const int e = find_group(p.tprefix, p.tscale, p.groups, L);
+    const int q = L - p.tprefix[e] * p.tscale;
+    const int off = p.offsets[e];
+    const int cnt = p.offsets[e + 1] - off;
+    int m0, n0, mvalid, kvalid;
+    if constexpr (GM == GROUP_M) {
+      const int mt_e = (cnt + BM - 1) / BM;
+      m0 = (q % mt_e) * BM; n0 = (q / mt_e) * BN;
+      mvalid = cnt - m0; kvalid = p.K;
+    } else {
+      m0 = (q / NTILES) * BM; n0 = (q % NTILES) * BN;
+      mvalid = p.M - m0; kvalid = cnt;
+    }
+    const int nvalid = p.N - n0;
+    const int nk = (kvalid + BK - 1) / BK;
+    // operand bases at k = 0
+    const bf16* Ab;
+    const bf16* Bb;
+    if constexpr (GM == GROUP_M) Ab = p.A + (int64_t)(off + m0) * p.lda;
+    else Ab = p.A + (int64_t)off * p.lda + m0;
+    if constexpr (GM == GROUP_M)
+      Bb = p.B + (int64_t)e * p.b_gstride + (B_T ? (int64_t)n0 : (int64_t)n0 * p.ldb);
+    else
+      Bb = p.B + (int64_t)off * p.ldb + n0;
+
+    auto issue = [&](int kt) {
+      char* buf = smem + (kt % STAGES) * SBYTES;
+      const int k0 = kt * BK;
+      if constexpr (A_T) TA::load(Ab + (int64_t)k0 * p.lda, p.lda, mvalid, kvalid - k0, buf, wave, lane);
+      else TA::load(Ab + k0, p.lda, mvalid, buf, wave, lane);
+      if constexpr (B_T) TB::load(Bb + (int64_t)k0 * p.ldb, p.ldb, nvalid, kvalid - k0, buf + ABYTES, wave, lane);
+      else TB::load(Bb + k0, p.ldb, nvalid, buf + ABYTES, wave, lane);
+    };
+    constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave (upper bound)
+
+    f32x16_t acc[TN][TM];
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int j = 0; j < TM; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < nk) issue(s);
+
+    for (int kt = 0; kt < nk; ++kt) {
+      const int ahead = nk - 1 - kt;                  // stages issued after kt (capped below)
+      if constexpr (STAGES >= 4) {
+        if (ahead >= 2) wait_vmcnt<2 * LPS>(); else if (ahead == 1) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
+      } else if constexpr (STAGES == 3) {
+        if (ahead >= 1) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      char* buf = smem + (kt % STAGES) * SBYTES;
+      if constexpr (GM == GROUP_K) {
+        const int kv = kvalid - kt * BK;
+        if (kv < BK) {                                // zero the k rows past the expert's tokens
+          block_sync_lds();                            // (after every wave's loads of this stage landed)
+          TA::zero_tail(buf, kv, tid, NT);
+          TB::zero_tail(buf + ABYTES, kv, tid, NT);
+        }
+      }
+      block_sync_lds();
+      if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+      const char* as = buf;
+      const char* bs = buf + ABYTES;
+#pragma unroll
+      for (int kk = 0; kk < BK; kk += 16) {
+        bf16x8_t fa[TM], fb[TN];
+#pragma unroll
+        for (int j = 0; j < TM; ++j) {
+          if constexpr (A_T) fa[j] = TA::frag(as, wm * WTM + j * 32, kk, lane);
+          else fa[j] = TA::frag(as, wm * WTM + j * 32, kk / 8, lane);
+        }
+#pragma unroll
+        for (int i = 0; i < TN; ++i) {
+          if constexpr (B_T) fb[i] = TB::frag(bs, wn * WTN + i * 32, kk, lane);
+          else fb[i] = TB::frag(bs, wn * WTN + i * 32, kk / 8, lane);
+        }
+#pragma unroll
+        for (int i = 0; i < TN; ++i)
+#pragma unroll
+          for (int j = 0; j < TM; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[i], fa[j], acc[i][j], 0, 0, 0);
+      }
+    }
+    block_sync_lds();      // every wave is done with the ring before the next tile's loads
+
+    // epilogue (same accumulator layout as grouped_gemm)
+    const int l32 = lane & 31, lhi = lane >> 5;
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int ml = wm * WTM + j * 32 + l32;
+      if (ml >= mvalid) continue;
+      int64_t crow;
+      if constexpr (GM == GROUP_M) crow = (int64_t)(off + m0 + ml) * p.ldc;
+      else crow = (int64_t)e * p.c_gstride + (int64_t)(m0 + ml) * p.ldc;
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int nl = wn * WTN + i * 32 + 8 * g + 4 * lhi;
+          if (nl >= nvalid) continue;
+          const int n = n0 + nl;
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * g + r];
+          if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_ACT) {
+            const bf16* bp = p.bias + (int64_t)e * p.bias_gstride + n;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] += bf2f(bp[r]);
+          }
+          if constexpr (EPI == EPI_DACT) {
+            const bf16* hp = p.aux + crow + n;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] *= act_bwd(bf2f(hp[r]), p.act);
+          }
+          if constexpr (EPI == EPI_F32) {
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) = make_float4(v[0], v[1], v[2], v[3]);
+          } else {
+            bf16* cp = reinterpret_cast<bf16*>(p.C) + crow + n;
+            *reinterpret_cast<uint2*>(cp) = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                                                       (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+            if constexpr (EPI == EPI_BIAS_ACT) {
+              float a[4];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) a[r] = act_fwd(v[r], p.act);
+              bf16* ap = reinterpret_cast<bf16*>(p.C2) + crow + n;
+              *reinterpret_cast<uint2*>(ap) = make_uint2((uint32_t)f2bf(a[0]) | ((uint32_t)f2bf(a[1]) << 16),
+                                                         (uint32_t)f2bf(a[2]) | ((uint32_t)f2bf(a[3]) << 16));
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int STAGES, bool A_T, bool B_T>
+constexpr size_t gemm2_lds_bytes() {
+  return (size_t)STAGES * ((A_T ? 64 * BM * 2 : BM * 128) + (B_T ? 64 * BN * 2 : BN * 128));
+}
+
+}  // namespace dmoe
