@@ -23,12 +23,12 @@ from .dmoe import (
     to64, gate_scores, decision_scores, flat_index, uid_of, cell_totals,
     topk_bruteforce, topk_beam, topk_product_key, mixture_weights, act, act_grad,
     dispatch, expert_forward, expert_backward, gate_backward, layer_forward,
-    layer_backward, routing, chosen_totals, round_bf16,
+    layer_backward, routing, chosen_totals, round_bf16, expert_forward_stored,
 )
 
 __all__ = [
     "to64", "gate_scores", "decision_scores", "flat_index", "uid_of", "cell_totals",
     "topk_bruteforce", "topk_beam", "topk_product_key", "mixture_weights", "act",
     "act_grad", "dispatch", "expert_forward", "expert_backward", "gate_backward",
-    "layer_forward", "layer_backward", "routing", "chosen_totals", "round_bf16",
+    "layer_forward", "layer_backward", "routing", "chosen_totals", "round_bf16", "expert_forward_stored",
 ]

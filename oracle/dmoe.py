@@ -219,6 +219,16 @@ def expert_forward(X, W1, b1, W2, b2, kind):
     return h, a, y
 
 
+def expert_forward_stored(X, W1, b1, W2, b2, kind, store=None):
+    """expert_forward as a layer with storage dtype `store` keeps it: the activation
+    is computed from the exact pre-activation, then h and a are rounded, and the
+    output is computed from the rounded a and rounded in turn."""
+    store = store or _identity
+    h = X @ W1.T + b1[None, :]
+    a = store(act(h, kind))
+    return store(h), a, store(a @ W2.T + b2[None, :])
+
+
 def expert_backward(X, h, a, dY, W1, W2, kind, store=None):
     """Gradients of the expert block for a batch: (dX, dW1, db1, dW2, db2).
     store (optional) rounds the tensors a layer keeps in its storage dtype:
@@ -307,10 +317,7 @@ def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, s
     for e in todo:
         lo, hi = offsets[e], offsets[e + 1]
         W1, b1, W2, b2 = get(e)
-        he = x[row_token[lo:hi]] @ W1.T + b1[None, :]
-        ae = store(act(he, kind))
-        he = store(he)
-        ye = store(ae @ W2.T + b2[None, :])
+        he, ae, ye = expert_forward_stored(x[row_token[lo:hi]], W1, b1, W2, b2, kind, store)
         hs[e], as_[e] = he, ae
         y_perm[lo:hi] = ye
     if hs:
