@@ -104,12 +104,12 @@ static void run_gemm(GemmArgs<E> p, int64_t tiles_ub, hipStream_t st) {
 }
 
 // gfx950 bf16 path: direct-to-LDS multi-stage GEMM (gemm2.hpp)
-template <int GM, bool AT, bool BT, int EPI, int BM, int BN, int WM, int WN, int ST>
+template <int GM, bool AT, bool BT, int EPI, int BM, int BN, int WM, int WN, int ST, int BK>
 static void run_gemm2(GemmArgs<bf16> p, int64_t tiles_ub, hipStream_t st) {
   if (tiles_ub <= 0) return;
-  auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1>;
+  auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1, BK>;
   constexpr int NT = 64 * WM * WN;
-  const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT>();
+  const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT, BK>();
   static int per_cu = 0;
   if (!per_cu) {
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -136,10 +136,11 @@ struct CfgF32    { static constexpr int BM = 32, BN = 64, BK = 32, WM = 1, WN = 
 struct CfgDWF32  { static constexpr int BM = 64, BN = 64, BK = 32, WM = 2, WN = 2; };
 
 // bf16 tile shapes of the gemm2 path: many rows per expert -> 256x256 tiles, 8 waves,
-// 2 stages (MFMA-bound); few rows -> 32x256 tiles, 4 waves, 4 stages (weight streaming).
-struct G2Fat    { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2; };
-struct G2Skinny { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4; };
-struct G2DW     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2; };
+// 64-deep k, 2 stages (best of the measured shapes at the wide workload for all three
+// operand layouts); few rows -> 32x256 tiles, 4 waves, 4 stages (weight streaming).
+struct G2Fat    { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
+struct G2Skinny { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4, BK = 64; };
+struct G2DW     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
 
 template <typename C>
 static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, const bf16* W1,
@@ -156,7 +157,7 @@ static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.C = h; p.ldc = H; p.C2 = a;
     p.bias = b1; p.bias_gstride = H;
     p.N = H; p.K = D; p.act = s.act;
-    run_gemm2<GROUP_M, false, false, EPI_BIAS_ACT, C::BM, C::BN, C::WM, C::WN, C::ST>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, false, EPI_BIAS_ACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
   }
   {
     const int nt = (D + C::BN - 1) / C::BN;
@@ -166,7 +167,7 @@ static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.C = yp; p.ldc = D;
     p.bias = b2; p.bias_gstride = D;
     p.N = D; p.K = H; p.act = s.act;
-    run_gemm2<GROUP_M, false, false, EPI_BIAS, C::BM, C::BN, C::WM, C::WN, C::ST>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, false, EPI_BIAS, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
   }
 }
 
@@ -186,7 +187,7 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
     p.C = dh; p.ldc = H; p.aux = h;
     p.N = H; p.K = D; p.act = s.act;
-    run_gemm2<GROUP_M, false, true, EPI_DACT, C::BM, C::BN, C::WM, C::WN, C::ST>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, true, EPI_DACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
   }
   {   // dW2_e = dy_e^T a_e   [D, H]
     const int mt = (D + CW::BM - 1) / CW::BM, nt = (H + CW::BN - 1) / CW::BN;
@@ -195,7 +196,7 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.B = a; p.ldb = H;
     p.C = dW2; p.ldc = H; p.c_gstride = (int64_t)D * H;
     p.M = D; p.N = H; p.act = s.act;
-    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST>(p, active_ub * mt * nt, st);
+    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
   }
   {   // dx_perm = dh W1: W1_e read as (n = d, k = h), N-contiguous
     const int nt = (D + C::BN - 1) / C::BN;
@@ -204,7 +205,7 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
     p.C = dxp; p.ldc = D;
     p.N = D; p.K = H; p.act = s.act;
-    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
   }
   {   // dW1_e = dh_e^T x_e   [H, D]
     const int mt = (H + CW::BM - 1) / CW::BM, nt = (D + CW::BN - 1) / CW::BN;
@@ -213,7 +214,7 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.B = xp; p.ldb = D;
     p.C = dW1; p.ldc = D; p.c_gstride = (int64_t)H * D;
     p.M = H; p.N = D; p.act = s.act;
-    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST>(p, active_ub * mt * nt, st);
+    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
   }
   hipLaunchKernelGGL(segment_colsum<bf16>, dim3((unsigned)((H / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
                      st, dh, (int64_t)H, offsets, H, db1);

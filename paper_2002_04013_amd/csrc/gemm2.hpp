@@ -10,9 +10,9 @@
 //   A_T = false: A[m][k] at A[m*lda + k]        A_T = true: A[m][k] at A[k*lda + m]
 //   B_T = false: B[n][k] at B[n*ldb + k]        B_T = true: B[n][k] at B[k*ldb + n]
 //
-// LDS tile layouts (bf16, 16-byte chunks):
-//   K-contiguous tile [R][BK=64]: row r holds 8 chunks; chunk c of row r is stored
-//     at position c ^ swz(r).  A wave's load instruction fills 8 whole rows.
+// LDS tile layouts (bf16, 16-byte chunks; BK = 32 or 64):
+//   K-contiguous tile [R][BK]: row r holds BK/8 chunks; chunk c of row r is stored
+//     at position c ^ swz(r).  A wave's load instruction fills 1024/(2 BK) whole rows.
 //   N-contiguous tile [BK][R]: row k holds R/8 chunks; chunk c of row k is stored
 //     at position c ^ (4 * (k % 4)) (R >= 128).  An instruction fills 1024/(2R) rows.
 // Rows beyond the valid m/n range are loaded from a clamped address (their output
@@ -45,16 +45,27 @@ __device__ __forceinline__ void block_sync_lds() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int SW>
-__device__ __forceinline__ int swz_kc(int r) { return SW == 0 ? (r & 7) : ((r >> 1) & 7); }
+// Chunk swizzle of a K-contiguous tile.  BK = 64 (8 chunks, 128-byte rows):
+// position = chunk ^ (r % 8) or ^ ((r / 2) % 8).  BK = 32 (4 chunks, 64-byte rows):
+// position = chunk ^ ((r / 4) % 4), which makes any 16 consecutive rows read at one
+// chunk fall on 16 distinct 16-byte bank groups.
+template <int BK, int SW>
+__device__ __forceinline__ int swz_kc(int r) {
+  if constexpr (BK == 32) return (r >> 2) & 3;
+  return SW == 0 ? (r & 7) : ((r >> 1) & 7);
+}
 
-// ---- K-contiguous tile [R][64] -------------------------------------------------------
-template <int R, int NW, int SW>
+// ---- K-contiguous tile [R][BK] -------------------------------------------------------
+template <int R, int NW, int SW, int BK>
 struct KcTile {
-  static constexpr int BYTES = R * 128;
-  static constexpr int INSTR = R / 8;                  // 1 KB wave instructions per tile
+  static constexpr int RB = BK * 2;                    // bytes per row
+  static constexpr int CH = BK / 8;                    // chunks per row
+  static constexpr int RPI = 1024 / RB;                // rows per wave instruction
+  static constexpr int BYTES = R * RB;
+  static constexpr int INSTR = R / RPI;                // 1 KB wave instructions per tile
   static constexpr int PER_WAVE = (INSTR + NW - 1) / NW;
-  static_assert(R % 8 == 0, "rows");
+  static_assert(BK == 32 || BK == 64, "BK");
+  static_assert(R % RPI == 0, "rows");
   // issue this wave's loads: rows [0, R) of the tile starting at `base` (row stride ld)
   __device__ __forceinline__ static void load(const bf16* base, int64_t ld, int rvalid, char* lds, int wave,
                                               int lane) {
@@ -62,8 +73,8 @@ struct KcTile {
     for (int i = 0; i < PER_WAVE; ++i) {
       const int q = wave + i * NW;
       if (INSTR % NW != 0 && q >= INSTR) break;
-      const int r = q * 8 + (lane >> 3);
-      const int c = (lane & 7) ^ swz_kc<SW>(r);
+      const int r = q * RPI + lane / CH;
+      const int c = (lane % CH) ^ swz_kc<BK, SW>(r);
       const int rr = r < rvalid ? r : rvalid - 1;
       g2l_16(base + (int64_t)rr * ld + c * 8, lds + q * 1024);
     }
@@ -71,18 +82,18 @@ struct KcTile {
   // fragment of rows r0 + (lane % 32), k chunk kc + lane / 32 (8 bf16)
   __device__ __forceinline__ static bf16x8_t frag(const char* lds, int r0, int kc, int lane) {
     const int r = r0 + (lane & 31);
-    const int c = (kc + (lane >> 5)) ^ swz_kc<SW>(r);
-    return *reinterpret_cast<const bf16x8_t*>(lds + r * 128 + c * 16);
+    const int c = (kc + (lane >> 5)) ^ swz_kc<BK, SW>(r);
+    return *reinterpret_cast<const bf16x8_t*>(lds + r * RB + c * 16);
   }
 };
 
-// ---- N-contiguous tile [64][R] (row = k) ---------------------------------------------
-template <int R, int NW>
+// ---- N-contiguous tile [BK][R] (row = k) ---------------------------------------------
+template <int R, int NW, int BK>
 struct NcTile {
-  static constexpr int BYTES = 64 * R * 2;
+  static constexpr int BYTES = BK * R * 2;
   static constexpr int CPR = R / 8;                    // chunks per row
   static constexpr int RPI = 1024 / (R * 2);           // rows per wave instruction
-  static constexpr int INSTR = 64 / RPI;
+  static constexpr int INSTR = BK / RPI;
   static constexpr int PER_WAVE = (INSTR + NW - 1) / NW;
   static_assert(R >= 128 && R <= 512 && (R & (R - 1)) == 0, "cols");
   __device__ __forceinline__ static int swz(int k) { return 4 * (k & 3); }
@@ -102,10 +113,10 @@ struct NcTile {
       g2l_16(base + (int64_t)kk * ld + col, lds + q * 1024);
     }
   }
-  // zero rows [kvalid, 64) of the tile (GROUP_K tail)
+  // zero rows [kvalid, BK) of the tile (GROUP_K tail)
   __device__ __forceinline__ static void zero_tail(char* lds, int kvalid, int tid, int nt) {
     uint4* p = reinterpret_cast<uint4*>(lds + kvalid * R * 2);
-    const int n = (64 - kvalid) * CPR;
+    const int n = (BK - kvalid) * CPR;
     for (int i = tid; i < n; i += nt) p[i] = make_uint4(0, 0, 0, 0);
   }
   // MFMA fragment for columns c0 .. c0+31 (lane % 32) and k = kk .. kk+15 (lane / 32 picks 8):
@@ -131,14 +142,14 @@ struct NcTile {
   }
 };
 
-template <int GM, bool A_T, bool B_T, int EPI, int BM, int BN, int WM, int WN, int STAGES, int SW>
+template <int GM, bool A_T, bool B_T, int EPI, int BM, int BN, int WM, int WN, int STAGES, int SW, int BK>
 __global__ void __launch_bounds__(64 * WM * WN)
 grouped_gemm2(GemmArgs<bf16> p) {
-  constexpr int NW = WM * WN, NT = 64 * NW, BK = 64;
+  constexpr int NW = WM * WN, NT = 64 * NW;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  using TA = typename std::conditional<A_T, NcTile<BM, NW>, KcTile<BM, NW, SW>>::type;
-  using TB = typename std::conditional<B_T, NcTile<BN, NW>, KcTile<BN, NW, SW>>::type;
+  using TA = typename std::conditional<A_T, NcTile<BM, NW, BK>, KcTile<BM, NW, SW, BK>>::type;
+  using TB = typename std::conditional<B_T, NcTile<BN, NW, BK>, KcTile<BN, NW, SW, BK>>::type;
   constexpr int ABYTES = TA::BYTES, SBYTES = TA::BYTES + TB::BYTES;
   static_assert(TM >= 1 && TN >= 1, "tile");
   static_assert(TA::INSTR % NW == 0 && TB::INSTR % NW == 0, "equal load counts per wave");
@@ -148,7 +159,10 @@ grouped_gemm2(GemmArgs<bf16> p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave % WM, wn = wave / WM;
+  // Waves go to the 4 SIMDs round-robin; with wm = wave / WN the two waves sharing a
+  // SIMD cover different row ranges, so in a partly filled m-tile (the last tile of
+  // an expert) the wave with no rows left hands its SIMD's matrix core to the other.
+  const int wm = wave / WN, wn = wave % WN;
 
   const int total = p.tprefix[p.groups] * p.tscale;
   int L, Lend, Lstep;
@@ -162,41 +176,73 @@ grouped_gemm2(GemmArgs<bf16> p) {
   }
   const int NTILES = (p.N + BN - 1) / BN;
 
-  for (; L < Lend; L += Lstep) {
-    const int e = find_group(p.tprefix, p.tscale, p.groups, L);
-    const int q = L - p.tprefix[e] * p.tscale;
-    const int off = p.offsets[e];
-    const int cnt = p.offsets[e + 1] - off;
-    int m0, n0, mvalid, kvalid;
-    if constexpr (GM == GROUP_M) {
-      const int mt_e = (cnt + BM - 1) / BM;
-      m0 = (q % mt_e) * BM; n0 = (q / mt_e) * BN;
-      mvalid = cnt - m0; kvalid = p.K;
-    } else {
-      m0 = (q / NTILES) * BM; n0 = (q % NTILES) * BN;
-      mvalid = p.M - m0; kvalid = cnt;
-    }
-    const int nvalid = p.N - n0;
-    const int nk = (kvalid + BK - 1) / BK;
-    // operand bases at k = 0
+  // Coordinates and operand bases of tile L.
+  struct TileC {
+    int e, off, m0, n0, mvalid, nvalid, kvalid, nk;
     const bf16* Ab;
     const bf16* Bb;
-    if constexpr (GM == GROUP_M) Ab = p.A + (int64_t)(off + m0) * p.lda;
-    else Ab = p.A + (int64_t)off * p.lda + m0;
-    if constexpr (GM == GROUP_M)
-      Bb = p.B + (int64_t)e * p.b_gstride + (B_T ? (int64_t)n0 : (int64_t)n0 * p.ldb);
-    else
-      Bb = p.B + (int64_t)off * p.ldb + n0;
+  };
+  auto setup = [&](int Lt) {
+    TileC t;
+    t.e = find_group(p.tprefix, p.tscale, p.groups, Lt);
+    const int q = Lt - p.tprefix[t.e] * p.tscale;
+    t.off = p.offsets[t.e];
+    const int cnt = p.offsets[t.e + 1] - t.off;
+    if constexpr (GM == GROUP_M) {
+      const int mt_e = (cnt + BM - 1) / BM;
+      t.m0 = (q % mt_e) * BM; t.n0 = (q / mt_e) * BN;
+      t.mvalid = cnt - t.m0; t.kvalid = p.K;
+      t.Ab = p.A + (int64_t)(t.off + t.m0) * p.lda;
+      t.Bb = p.B + (int64_t)t.e * p.b_gstride + (B_T ? (int64_t)t.n0 : (int64_t)t.n0 * p.ldb);
+    } else {
+      // grouped order: consecutive tiles walk GMT m-tiles, then the next n-tile, so the
+      // tiles in flight on one XCD share a few A and B slabs (fits its L2)
+      constexpr int GMT = 4;
+      const int MTILES = (p.M + BM - 1) / BM;
+      const int per_group = GMT * NTILES;
+      const int first = (q / per_group) * GMT;
+      const int gsize = MTILES - first < GMT ? MTILES - first : GMT;
+      const int qi = q % per_group;
+      t.m0 = (first + qi % gsize) * BM; t.n0 = (qi / gsize) * BN;
+      t.mvalid = p.M - t.m0; t.kvalid = cnt;
+      t.Ab = p.A + (int64_t)t.off * p.lda + t.m0;
+      t.Bb = p.B + (int64_t)t.off * p.ldb + t.n0;
+    }
+    t.nvalid = p.N - t.n0;
+    t.nk = (t.kvalid + BK - 1) / BK;
+    return t;
+  };
+  auto issue = [&](const TileC& t, int kt) {
+    char* buf = smem + (kt % STAGES) * SBYTES;
+    const int k0 = kt * BK;
+    if constexpr (A_T) TA::load(t.Ab + (int64_t)k0 * p.lda, p.lda, t.mvalid, t.kvalid - k0, buf, wave, lane);
+    else TA::load(t.Ab + k0, p.lda, t.mvalid, buf, wave, lane);
+    if constexpr (B_T) TB::load(t.Bb + (int64_t)k0 * p.ldb, p.ldb, t.nvalid, t.kvalid - k0, buf + ABYTES, wave, lane);
+    else TB::load(t.Bb + k0, p.ldb, t.nvalid, buf + ABYTES, wave, lane);
+  };
+  auto prologue = [&](const TileC& t) {
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < t.nk) issue(t, s);
+  };
+  constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave
 
-    auto issue = [&](int kt) {
-      char* buf = smem + (kt % STAGES) * SBYTES;
-      const int k0 = kt * BK;
-      if constexpr (A_T) TA::load(Ab + (int64_t)k0 * p.lda, p.lda, mvalid, kvalid - k0, buf, wave, lane);
-      else TA::load(Ab + k0, p.lda, mvalid, buf, wave, lane);
-      if constexpr (B_T) TB::load(Bb + (int64_t)k0 * p.ldb, p.ldb, nvalid, kvalid - k0, buf + ABYTES, wave, lane);
-      else TB::load(Bb + k0, p.ldb, nvalid, buf + ABYTES, wave, lane);
-    };
-    constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave (upper bound)
+  // The first stages of a tile are issued before the previous tile's epilogue, so
+  // their latency overlaps its arithmetic and stores.
+  TileC nxt{};
+  if (L < Lend) {
+    wait_vmcnt<0>();
+    nxt = setup(L);
+    prologue(nxt);
+  }
+  for (; L < Lend; L += Lstep) {
+    const TileC t = nxt;
+    const int e = t.e, off = t.off, m0 = t.m0, n0 = t.n0, mvalid = t.mvalid, nvalid = t.nvalid;
+    const int kvalid = t.kvalid, nk = t.nk;
+    // 32-row blocks of this wave that hold rows of the tile (wave-uniform)
+    bool jlive[TM];
+#pragma unroll
+    for (int j = 0; j < TM; ++j) jlive[j] = wm * WTM + j * 32 < mvalid;
 
     f32x16_t acc[TN][TM];
 #pragma unroll
@@ -206,14 +252,13 @@ grouped_gemm2(GemmArgs<bf16> p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    wait_vmcnt<0>();
-#pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
-      if (s < nk) issue(s);
-
     for (int kt = 0; kt < nk; ++kt) {
+      // stage kt must have landed.  At kt = 0 everything outstanding is drained: the
+      // prologue of this tile and the previous tile's epilogue stores.
       const int ahead = nk - 1 - kt;                  // stages issued after kt (capped below)
-      if constexpr (STAGES >= 4) {
+      if (kt == 0) {
+        wait_vmcnt<0>();
+      } else if constexpr (STAGES >= 4) {
         if (ahead >= 2) wait_vmcnt<2 * LPS>(); else if (ahead == 1) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
       } else if constexpr (STAGES == 3) {
         if (ahead >= 1) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
@@ -230,30 +275,54 @@ grouped_gemm2(GemmArgs<bf16> p) {
         }
       }
       block_sync_lds();
-      if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+      if (kt + STAGES - 1 < nk) issue(t, kt + STAGES - 1);
       const char* as = buf;
       const char* bs = buf + ABYTES;
-#pragma unroll
-      for (int kk = 0; kk < BK; kk += 16) {
-        bf16x8_t fa[TM], fb[TN];
+      // Fragments are double-buffered across the 16-deep k steps: the reads for step
+      // kk+1 are issued before the MFMAs of step kk, and the scheduler is asked to
+      // interleave the two so LDS latency hides behind matrix work.
+      constexpr int KK = BK / 16;
+      constexpr int NDS = (A_T ? 2 : 1) * TM + (B_T ? 2 : 1) * TN;   // LDS reads per step
+      bf16x8_t fa[2][TM], fb[2][TN];
+      auto ldfrag = [&](int kk, bf16x8_t* A_, bf16x8_t* B_) {
 #pragma unroll
         for (int j = 0; j < TM; ++j) {
-          if constexpr (A_T) fa[j] = TA::frag(as, wm * WTM + j * 32, kk, lane);
-          else fa[j] = TA::frag(as, wm * WTM + j * 32, kk / 8, lane);
+          if (!jlive[j]) continue;
+          if constexpr (A_T) A_[j] = TA::frag(as, wm * WTM + j * 32, kk * 16, lane);
+          else A_[j] = TA::frag(as, wm * WTM + j * 32, kk * 2, lane);
         }
 #pragma unroll
         for (int i = 0; i < TN; ++i) {
-          if constexpr (B_T) fb[i] = TB::frag(bs, wn * WTN + i * 32, kk, lane);
-          else fb[i] = TB::frag(bs, wn * WTN + i * 32, kk / 8, lane);
+          if constexpr (B_T) B_[i] = TB::frag(bs, wn * WTN + i * 32, kk * 16, lane);
+          else B_[i] = TB::frag(bs, wn * WTN + i * 32, kk * 2, lane);
         }
+      };
+      ldfrag(0, fa[0], fb[0]);
 #pragma unroll
-        for (int i = 0; i < TN; ++i)
+      for (int kk = 0; kk < KK; ++kk) {
+        const int cb = kk & 1;
+        if (kk + 1 < KK) ldfrag(kk + 1, fa[cb ^ 1], fb[cb ^ 1]);
 #pragma unroll
-          for (int j = 0; j < TM; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[i], fa[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TM; ++j) {
+          if (!jlive[j]) continue;
+#pragma unroll
+          for (int i = 0; i < TN; ++i)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cb][i], fa[cb][j], acc[i][j], 0, 0, 0);
+        }
+        if (kk + 1 < KK) {
+#pragma unroll
+          for (int q = 0; q < TM * TN; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // one MFMA
+            if (q < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+          }
+        }
       }
     }
     block_sync_lds();      // every wave is done with the ring before the next tile's loads
+    if (L + Lstep < Lend) {
+      nxt = setup(L + Lstep);
+      prologue(nxt);
+    }
 
     // epilogue (same accumulator layout as grouped_gemm)
     const int l32 = lane & 31, lhi = lane >> 5;
@@ -305,9 +374,9 @@ grouped_gemm2(GemmArgs<bf16> p) {
   }
 }
 
-template <int BM, int BN, int STAGES, bool A_T, bool B_T>
+template <int BM, int BN, int STAGES, bool A_T, bool B_T, int BK>
 constexpr size_t gemm2_lds_bytes() {
-  return (size_t)STAGES * ((A_T ? 64 * BM * 2 : BM * 128) + (B_T ? 64 * BN * 2 : BN * 128));
+  return (size_t)STAGES * (BM + BN) * BK * 2;
 }
 
 }  // namespace dmoe

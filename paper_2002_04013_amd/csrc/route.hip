@@ -7,7 +7,7 @@
 //      each block's starting row per expert;
 //   3. each block ranks its pairs within every expert in pair order (wave-wide
 //      rank by lane comparison, waves taken in order) and writes pos/row_token;
-//   4. rows of x are gathered into x_perm with 16-byte vector copies.
+//   4. each token's row of x is copied to its alive pairs' rows of x_perm.
 #include "common.hpp"
 
 namespace dmoe {
@@ -105,18 +105,22 @@ dispatch_scatter(const int32_t* idx, const uint8_t* alive, int P, int N, int k,
   }
 }
 
+// x_perm[pos[t,j]] = x[t]: each token's row is read once and written to each of its
+// alive pairs' rows (reading per token, not per row, keeps x traffic at one pass).
 template <typename E>
 __global__ void __launch_bounds__(RT_NT)
-gather_rows(const E* x, const int32_t* row_token, const int32_t* offsets, int N, int D, E* xp) {
+gather_rows(const E* x, const int32_t* pos, int T, int k, int D, E* xp) {
   constexpr int VEC = 16 / sizeof(E);
   const int CPR = D / VEC;
-  const int64_t total = (int64_t)offsets[N] * CPR;
+  const int64_t total = (int64_t)T * CPR;
   for (int64_t q = (int64_t)blockIdx.x * RT_NT + threadIdx.x; q < total; q += (int64_t)gridDim.x * RT_NT) {
-    const int64_t r = q / CPR;
+    const int64_t t = q / CPR;
     const int c = (int)(q % CPR);
-    const int t = row_token[r];
-    *reinterpret_cast<uint4*>(xp + r * D + c * VEC) =
-        *reinterpret_cast<const uint4*>(x + (int64_t)t * D + c * VEC);
+    const uint4 v = *reinterpret_cast<const uint4*>(x + t * D + c * VEC);
+    for (int j = 0; j < k; ++j) {
+      const int r = pos[t * k + j];
+      if (r >= 0) *reinterpret_cast<uint4*>(xp + (int64_t)r * D + c * VEC) = v;
+    }
   }
 }
 
@@ -257,14 +261,14 @@ extern "C" int dmoe_dispatch(const dmoe_dims* dims, const void* x, const int32_t
   if (nb == 0) return launch_status();
   hipLaunchKernelGGL(dispatch_scatter, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N,
                      s.k, bh, pos, row_token);
-  const int64_t chunks = s.P * (s.D * (int64_t)s.esz / 16);
+  const int64_t chunks = s.T * (s.D * (int64_t)s.esz / 16);
   const int grid = (int)std::min<int64_t>((chunks + RT_NT - 1) / RT_NT, 256 * 16);
   if (s.dtype == DMOE_BF16)
     hipLaunchKernelGGL(gather_rows<bf16>, dim3(grid), dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(x),
-                       row_token, offsets, N, (int)s.D, reinterpret_cast<bf16*>(x_perm));
+                       pos, (int)s.T, s.k, (int)s.D, reinterpret_cast<bf16*>(x_perm));
   else
     hipLaunchKernelGGL(gather_rows<float>, dim3(grid), dim3(RT_NT), 0, st, reinterpret_cast<const float*>(x),
-                       row_token, offsets, N, (int)s.D, reinterpret_cast<float*>(x_perm));
+                       pos, (int)s.T, s.k, (int)s.D, reinterpret_cast<float*>(x_perm));
   return launch_status();
 }
 
