@@ -58,8 +58,14 @@ typedef struct {
   int32_t k;      /* experts chosen per token */
   int32_t dtype;  /* DMOE_F32 or DMOE_BF16 */
   int32_t act;    /* DMOE_RELU or DMOE_GELU */
-  int32_t reserved;
+  int32_t flags;  /* 0, or DMOE_FLAG_* bits */
 } dmoe_dims;
+
+/* dmoe_dims.flags: DMOE_FLAG_GATE_EXACT makes dmoe_gate_topk compute every token's
+ * bf16 gate scores with exact fp64 accumulation (the path it otherwise takes only
+ * for tokens whose MFMA-computed decision is not certified).  Results are the same;
+ * only the speed differs. */
+enum { DMOE_FLAG_GATE_EXACT = 1 };
 
 /* Bytes of device workspace every entry point below needs for these dims
  * (one buffer of this size serves all of them; it may be reused between calls
@@ -82,8 +88,12 @@ const char* dmoe_strerror(int code);
  *                        every chosen expert is dead
  *   g      [T, k] fp32   chosen totals g(x, f), or NULL
  *   scores [T, d*M] fp32 per-dimension decision scores g_i(x), or NULL
- * Selection compares the fp32 rounding of each g_i(x)[u] (computed with fp64
- * accumulation) and adds the d fp32 values of a cell in fp64 in dim order.
+ * Selection compares the fp32 rounding of each exact score g_i(x)[u] and adds the d
+ * fp32 values of a cell in fp64 in dim order.  bf16: scores are computed on MFMA
+ * with a per-token error bound; a token whose TopK order is within the bound of a
+ * tie is recomputed with exact fp64 accumulation, so the selection equals the one
+ * of the exact scores; the returned scores, g and w carry the (bounded) MFMA error.
+ * fp32: exact fp64 accumulation for every token.
  * Uses workspace: no. */
 int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* Wg, const void* bg,
                    const uint8_t* alive, int32_t* idx, float* w, float* g, float* scores,

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(_PKG, "libdmoe.so")
 
 DMOE_F32, DMOE_BF16 = 0, 1
 DMOE_RELU, DMOE_GELU = 0, 1
+DMOE_FLAG_GATE_EXACT = 1
 
 # every extern "C" symbol the header declares
 EXPORTS = (
@@ -31,13 +32,13 @@ class DmoeError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int64), ("D", ctypes.c_int64), ("H", ctypes.c_int64),
                 ("d", ctypes.c_int32), ("M", ctypes.c_int32), ("k", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("flags", ctypes.c_int32)]
 
 
-def make_dims(T, D, H, d, M, k, dtype="bf16", act="gelu"):
+def make_dims(T, D, H, d, M, k, dtype="bf16", act="gelu", flags=0):
     return Dims(int(T), int(D), int(H), int(d), int(M), int(k),
                 DMOE_BF16 if dtype == "bf16" else DMOE_F32,
-                DMOE_GELU if act == "gelu" else DMOE_RELU, 0)
+                DMOE_GELU if act == "gelu" else DMOE_RELU, int(flags))
 
 
 _lib = None

@@ -11,6 +11,7 @@ int check_dims(const dmoe_dims* dims, Shape* s) {
   if (q.T < 0 || q.D <= 0 || q.H <= 0 || q.d < 1 || q.M < 1 || q.k < 1) return DMOE_EINVAL;
   if (q.dtype != DMOE_F32 && q.dtype != DMOE_BF16) return DMOE_EINVAL;
   if (q.act != DMOE_RELU && q.act != DMOE_GELU) return DMOE_EINVAL;
+  if (q.flags & ~DMOE_FLAG_GATE_EXACT) return DMOE_EINVAL;
   if (q.d > DMAX) return DMOE_EUNSUPPORTED;
   int64_t N = 1;
   for (int i = 0; i < q.d; ++i) {
@@ -23,7 +24,7 @@ int check_dims(const dmoe_dims* dims, Shape* s) {
   if (q.D % 64 || q.H % 64) return DMOE_EUNSUPPORTED;
   if (q.T * q.k > (int64_t)0x7fffffff / 2) return DMOE_EUNSUPPORTED;
   s->T = q.T; s->D = q.D; s->H = q.H; s->N = N; s->P = q.T * q.k; s->dM = (int64_t)q.d * q.M;
-  s->d = q.d; s->M = q.M; s->k = q.k; s->dtype = q.dtype; s->act = q.act;
+  s->d = q.d; s->M = q.M; s->k = q.k; s->dtype = q.dtype; s->act = q.act; s->flags = q.flags;
   s->esz = q.dtype == DMOE_BF16 ? 2 : 4;
   return DMOE_OK;
 }

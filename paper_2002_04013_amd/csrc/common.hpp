@@ -93,7 +93,7 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 struct Shape {
   int64_t T, D, H, N, P, dM;
-  int d, M, k, dtype, act;
+  int d, M, k, dtype, act, flags;
   size_t esz;   // bytes per element of the layer dtype
 };
 

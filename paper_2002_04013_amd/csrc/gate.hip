@@ -12,7 +12,7 @@ constexpr int GATE_NT = 256;
 struct GateArgs {
   const void* x; const void* Wg; const void* bg; const uint8_t* alive;
   int32_t* idx; float* w; float* g; float* scores;
-  int T, D, d, M, k, dM;
+  int T, D, d, M, k, dM, N;
 };
 
 // Insert (v, id) into a list sorted by (v desc, id asc) holding at most cap items.
@@ -62,7 +62,7 @@ __device__ void select_token(const double* s64, const uint8_t* alive,
     for (int i = 0; i < d; ++i) {
       cnt[i] = 0;
       for (int u = 0; u < M; ++u)
-        list_insert_f(lv + i * KMAX, li + i * KMAX, cnt[i], L, s32(i * M + u), u);
+        list_insert_f(lv + i * (KMAX + 1), li + i * (KMAX + 1), cnt[i], L, s32(i * M + u), u);
     }
     int ncand = 1;
     for (int i = 0; i < d; ++i) ncand *= L;
@@ -73,8 +73,8 @@ __device__ void select_token(const double* s64, const uint8_t* alive,
       if (prod > k) continue;
       double tot = 0.0;
       for (int i = 0; i < d; ++i) {
-        tot += (double)lv[i * KMAX + r[i]];
-        flat = flat * M + li[i * KMAX + r[i]];
+        tot += (double)lv[i * (KMAX + 1) + r[i]];
+        flat = flat * M + li[i * (KMAX + 1) + r[i]];
       }
       list_insert_d(tv, tf, nt, k, tot, flat);
     }
@@ -123,10 +123,10 @@ __global__ void __launch_bounds__(GATE_NT) gate_topk_kernel(GateArgs a) {
   double* xs = reinterpret_cast<double*>(sm);                         // [TB][KC]
   double* wsT = xs + GATE_TB * GATE_KC;                               // [KC][dM]
   double* s64 = wsT + GATE_KC * dM;                                   // [TB][dM]
-  float* lv = reinterpret_cast<float*>(s64 + GATE_TB * dM);           // [TB][DMAX*KMAX]
-  int* li = reinterpret_cast<int*>(lv + GATE_TB * DMAX * KMAX);       // [TB][DMAX*KMAX]
-  double* tv = reinterpret_cast<double*>(li + GATE_TB * DMAX * KMAX); // [TB][KMAX]
-  int* tf = reinterpret_cast<int*>(tv + GATE_TB * KMAX);              // [TB][KMAX]
+  float* lv = reinterpret_cast<float*>(s64 + GATE_TB * dM);                 // [TB][DMAX*(KMAX+1)]
+  int* li = reinterpret_cast<int*>(lv + GATE_TB * DMAX * (KMAX + 1));       // [TB][DMAX*(KMAX+1)]
+  double* tv = reinterpret_cast<double*>(li + GATE_TB * DMAX * (KMAX + 1)); // [TB][KMAX+1]
+  int* tf = reinterpret_cast<int*>(tv + GATE_TB * (KMAX + 1));              // [TB][KMAX+1]
 
   const int tid = threadIdx.x;
   const int t0 = blockIdx.x * GATE_TB;
@@ -190,16 +190,255 @@ __global__ void __launch_bounds__(GATE_NT) gate_topk_kernel(GateArgs a) {
   if (tid < GATE_TB && t0 + tid < a.T) {
     const int t = t0 + tid;
     select_token(s64 + tid * dM, a.alive, a.d, a.M, a.k,
-                 lv + tid * DMAX * KMAX, li + tid * DMAX * KMAX, tv + tid * KMAX, tf + tid * KMAX,
+                 lv + tid * DMAX * (KMAX + 1), li + tid * DMAX * (KMAX + 1), tv + tid * (KMAX + 1),
+                 tf + tid * (KMAX + 1),
                  a.idx + (int64_t)t * a.k, a.w + (int64_t)t * a.k,
                  a.g ? a.g + (int64_t)t * a.k : nullptr);
   }
 }
 
+// ---------------------------------------------------------------- bf16: MFMA scores + certificate
+//
+// Scores are computed on bf16 MFMA: products of bf16 values are exact in fp32, 64 of
+// them are summed per MFMA chunk in fp32, and the chunk sums are added in fp64.  A
+// second MFMA over |x|.|w| gives A = sum_k |x_k w_k|, which bounds the accumulation
+// error of each score:  |S - exact| <= delta = (gamma_64 + (D/64 + 8) 2^-52) A,
+// gamma_n = n u / (1 - n u) with u = 2^-23 (no assumption about the MFMA's internal
+// rounding beyond IEEE single precision operations).  Decision scores of the GPU and
+// of an exact computation then differ by at most delta + 1 ulp each, a cell total by
+// at most d (delta + ulp) =: E.  If the k+1 best cells (k when k = N) are separated
+// by gaps larger than 2E, the exact scores give the same TopK in the same order; such
+// tokens are certified.  The others are recomputed with exact fp64 accumulation.
+
+constexpr int GM_TOK = 32;        // tokens per block
+constexpr int GM_NT = 256;        // 4 waves, each a quarter of the d_model contraction
+
+struct GateMfmaArgs {
+  GateArgs a;
+  int flags;
+  float gam;                       // gamma_64 + (D/64+8) 2^-52, times 1/(1 - gamma_D)
+};
+
+// Certified selection of one token from its fp64 scores s64[dM] and error-bound sums
+// ab[dM].  Returns false (writes nothing) when the decision is not certified.
+__device__ bool select_token_cert(const double* s64, const float* ab, const uint8_t* alive, int d, int M,
+                                  int k, int N, float gam, float* lv, int* li, double* tv, int* tf,
+                                  int32_t* idx_out, float* w_out, float* g_out) {
+  const int K1 = k < N ? k + 1 : k;             // cells whose order must be certified
+  const int L = K1 < M ? K1 : M;
+  float amax = 0.f, amin = 3.4e38f, dmax = 0.f;
+  for (int c = 0; c < d * M; ++c) {
+    const float v = fabsf((float)s64[c]);
+    if (v > 0.f) { amax = fmaxf(amax, v); amin = fminf(amin, v); }
+    dmax = fmaxf(dmax, gam * ab[c]);
+  }
+  // fp64 totals of d fp32 values are exact when the magnitudes span < 2^25
+  if (amax > 0.f && amax > amin * 33554432.f) return false;
+  const double E = (double)d * ((double)dmax + (double)amax * 1.1920928955078125e-7);
+  int cnt[DMAX];
+  for (int i = 0; i < d; ++i) {
+    cnt[i] = 0;
+    for (int u = 0; u < M; ++u)
+      list_insert_f(lv + i * (KMAX + 1), li + i * (KMAX + 1), cnt[i], L, (float)s64[i * M + u], u);
+  }
+  int ncand = 1;
+  for (int i = 0; i < d; ++i) ncand *= L;
+  int nt = 0;
+  for (int q = 0; q < ncand; ++q) {
+    int rem = q, prod = 1, flat = 0;
+    int r[DMAX];
+    for (int i = d - 1; i >= 0; --i) { r[i] = rem % L; rem /= L; prod *= r[i] + 1; }
+    if (prod > K1) continue;
+    double tot = 0.0;
+    for (int i = 0; i < d; ++i) {
+      tot += (double)lv[i * (KMAX + 1) + r[i]];
+      flat = flat * M + li[i * (KMAX + 1) + r[i]];
+    }
+    list_insert_d(tv, tf, nt, K1, tot, flat);
+  }
+  for (int j = 0; j + 1 < K1; ++j)
+    if (!(tv[j] - tv[j + 1] > 2.0 * E)) return false;
+  // Eq. 1 weights from the fp64 totals of the chosen experts, over the alive ones
+  double gx[KMAX];
+  double m = -1.0e308;
+  bool any = false;
+  for (int j = 0; j < k; ++j) {
+    int rem = tf[j], u[DMAX];
+    for (int i = d - 1; i >= 0; --i) { u[i] = rem % M; rem /= M; }
+    double t = 0.0;
+    for (int i = 0; i < d; ++i) t += s64[i * M + u[i]];
+    gx[j] = t;
+    if (alive == nullptr || alive[tf[j]] != 0) { any = true; m = t > m ? t : m; }
+  }
+  float ex[KMAX];
+  float sum = 0.f;
+  for (int j = 0; j < k; ++j) {
+    const bool live = alive == nullptr || alive[tf[j]] != 0;
+    ex[j] = live ? expf((float)(gx[j] - m)) : 0.f;
+    sum += ex[j];
+  }
+  for (int j = 0; j < k; ++j) {
+    idx_out[j] = tf[j];
+    w_out[j] = any ? ex[j] / sum : 0.f;
+    if (g_out) g_out[j] = (float)gx[j];
+  }
+  return true;
+}
+
+__global__ void __launch_bounds__(GM_NT) gate_topk_mfma(GateMfmaArgs ga) {
+  const GateArgs& a = ga.a;
+  extern __shared__ __align__(16) unsigned char sm[];
+  const int dM = a.dM;
+  double* s64 = reinterpret_cast<double*>(sm);                               // [TOK][dM]
+  float* ab = reinterpret_cast<float*>(s64 + GM_TOK * dM);                   // [TOK][dM]
+  double* part = reinterpret_cast<double*>(ab + GM_TOK * dM);                // [GM_NT] fallback partials
+  float* lv = reinterpret_cast<float*>(part + GM_NT);                        // [TOK][DMAX*(KMAX+1)]
+  int* li = reinterpret_cast<int*>(lv + GM_TOK * DMAX * (KMAX + 1));
+  double* tv = reinterpret_cast<double*>(li + GM_TOK * DMAX * (KMAX + 1));   // [TOK][KMAX+1]
+  int* tf = reinterpret_cast<int*>(tv + GM_TOK * (KMAX + 1));
+  int* redo = tf + GM_TOK * (KMAX + 1);                                      // [TOK]
+  __shared__ int nredo;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * GM_TOK;
+  const bf16* x = reinterpret_cast<const bf16*>(a.x);
+  const bf16* W = reinterpret_cast<const bf16*>(a.Wg);
+  const bf16* bg = reinterpret_cast<const bf16*>(a.bg);
+  if (tid == 0) nredo = 0;
+  const int tok = lane & 31;                                   // token of this lane within the block
+  const int trow = min(t0 + tok, a.T - 1);
+  const int koff = 8 * (lane >> 5);
+  const int CB = (dM + 31) / 32;
+  const int KQ = a.D / 4;                                      // this wave's share of d_model
+  const int kbeg = wave * KQ;                                  // (D is a multiple of 64; KQ of 16)
+  const bool exact_all = (ga.flags & DMOE_FLAG_GATE_EXACT) != 0;
+  if (!exact_all) {
+    for (int cb = 0; cb < CB; ++cb) {
+      const int col = min(cb * 32 + (lane & 31), dM - 1);
+      const bf16* xr = x + (int64_t)trow * a.D + kbeg + koff;
+      const bf16* wr = W + (int64_t)col * a.D + kbeg + koff;
+      double acc[16];
+      f32x16_t aacc, c;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { acc[r] = 0.0; aacc[r] = 0.f; c[r] = 0.f; }
+      // chunks of 16 k; every 4 chunks (64 products) the fp32 sums move to fp64.
+      // loads run two chunks ahead of the MFMAs.
+      const int nch = KQ / 16;
+      uint4 xv[2], wv[2];
+      xv[0] = *reinterpret_cast<const uint4*>(xr);
+      wv[0] = *reinterpret_cast<const uint4*>(wr);
+      if (nch > 1) {
+        xv[1] = *reinterpret_cast<const uint4*>(xr + 16);
+        wv[1] = *reinterpret_cast<const uint4*>(wr + 16);
+      }
+      for (int q = 0; q < nch; ++q) {
+        const uint4 xq = xv[q & 1], wq = wv[q & 1];
+        if (q + 2 < nch) {
+          xv[q & 1] = *reinterpret_cast<const uint4*>(xr + 16 * (q + 2));
+          wv[q & 1] = *reinterpret_cast<const uint4*>(wr + 16 * (q + 2));
+        }
+        const uint4 xa = make_uint4(xq.x & 0x7fff7fffu, xq.y & 0x7fff7fffu, xq.z & 0x7fff7fffu, xq.w & 0x7fff7fffu);
+        const uint4 wa = make_uint4(wq.x & 0x7fff7fffu, wq.y & 0x7fff7fffu, wq.z & 0x7fff7fffu, wq.w & 0x7fff7fffu);
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wq), __builtin_bit_cast(bf16x8_t, xq),
+                                                   c, 0, 0, 0);
+        aacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wa),
+                                                      __builtin_bit_cast(bf16x8_t, xa), aacc, 0, 0, 0);
+        if ((q & 3) == 3 || q + 1 == nch) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) { acc[r] += (double)c[r]; c[r] = 0.f; }
+        }
+      }
+      // lane holds token (lane % 32) and columns cb*32 + 8(r/4) + 4(lane/32) + r%4; the four
+      // waves' partial sums are added in wave order
+      for (int w = 0; w < 4; ++w) {
+        if (wave == w) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int cc = cb * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (cc < dM) {
+              if (w == 0) {
+                s64[tok * dM + cc] = acc[r] + (bg ? (double)bf2f(bg[cc]) : 0.0);
+                ab[tok * dM + cc] = aacc[r];
+              } else {
+                s64[tok * dM + cc] += acc[r];
+                ab[tok * dM + cc] += aacc[r];
+              }
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+  }
+  __syncthreads();
+  // selection: one thread per token
+  if (tid < GM_TOK && t0 + tid < a.T) {
+    const int t = t0 + tid;
+    bool ok = false;
+    if (!exact_all)
+      ok = select_token_cert(s64 + tid * dM, ab + tid * dM, a.alive, a.d, a.M, a.k, a.N, ga.gam,
+                             lv + tid * DMAX * (KMAX + 1), li + tid * DMAX * (KMAX + 1),
+                             tv + tid * (KMAX + 1), tf + tid * (KMAX + 1), a.idx + (int64_t)t * a.k,
+                             a.w + (int64_t)t * a.k, a.g ? a.g + (int64_t)t * a.k : nullptr);
+    if (!ok) redo[atomicAdd(&nredo, 1)] = tid;
+  }
+  __syncthreads();
+  // tokens without a certificate: exact fp64 scores.  Thread tid takes column tid % dM
+  // and k-slice tid / dM of S = GM_NT / dM slices; slices are then added in order.
+  const int nr = nredo;
+  const int S = dM <= GM_NT ? GM_NT / dM : 1;
+  const int KS = (a.D / 8 + S - 1) / S * 8;                   // k per slice, multiple of 8
+  for (int i = 0; i < nr; ++i) {
+    const int tt = redo[i];
+    const int t = t0 + tt;
+    double sacc = 0.0;
+    const int c = tid % dM, sl = tid / dM;
+    if (sl < S) {
+      const bf16* xr = x + (int64_t)t * a.D;
+      const bf16* wr = W + (int64_t)c * a.D;
+      const int k1 = min(a.D, (sl + 1) * KS);
+      for (int kk = sl * KS; kk < k1; kk += 8) {
+        float xf[8], wf[8];
+        Vec<bf16>::unpack(*reinterpret_cast<const uint4*>(xr + kk), xf);
+        Vec<bf16>::unpack(*reinterpret_cast<const uint4*>(wr + kk), wf);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) sacc = fma((double)xf[q], (double)wf[q], sacc);
+      }
+    }
+    part[tid] = sacc;
+    __syncthreads();
+    if (tid < dM) {
+      double v = 0.0;
+      for (int q = 0; q < S; ++q) v += part[q * dM + tid];
+      s64[tt * dM + tid] = v + (bg ? (double)bf2f(bg[tid]) : 0.0);
+    }
+    __syncthreads();
+  }
+  if (tid < nr) {
+    const int tt = redo[tid];
+    const int t = t0 + tt;
+    select_token(s64 + tt * dM, a.alive, a.d, a.M, a.k, lv + tt * DMAX * (KMAX + 1), li + tt * DMAX * (KMAX + 1),
+                 tv + tt * (KMAX + 1), tf + tt * (KMAX + 1), a.idx + (int64_t)t * a.k, a.w + (int64_t)t * a.k,
+                 a.g ? a.g + (int64_t)t * a.k : nullptr);
+  }
+  if (a.scores) {
+    for (int q = tid; q < GM_TOK * dM; q += GM_NT) {
+      const int t = t0 + q / dM;
+      if (t < a.T) a.scores[(int64_t)t * dM + q % dM] = (float)s64[q];
+    }
+  }
+}
+
+static size_t gate_mfma_lds_bytes(int dM) {
+  return (sizeof(double) + sizeof(float)) * GM_TOK * dM + sizeof(double) * GM_NT +
+         (sizeof(float) + sizeof(int)) * GM_TOK * DMAX * (KMAX + 1) +
+         (sizeof(double) + sizeof(int)) * GM_TOK * (KMAX + 1) + sizeof(int) * GM_TOK;
+}
+
 static size_t gate_lds_bytes(int dM) {
   return sizeof(double) * (GATE_TB * GATE_KC + GATE_KC * dM + GATE_TB * dM) +
-         (sizeof(float) + sizeof(int)) * GATE_TB * DMAX * KMAX +
-         (sizeof(double) + sizeof(int)) * GATE_TB * KMAX;
+         (sizeof(float) + sizeof(int)) * GATE_TB * DMAX * (KMAX + 1) +
+         (sizeof(double) + sizeof(int)) * GATE_TB * (KMAX + 1);
 }
 
 // ---------------------------------------------------------------- backward
@@ -304,14 +543,29 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
   if (s.T == 0) return DMOE_OK;
   if (!x || !Wg || !idx || !w) return DMOE_EINVAL;
   if (!aligned16(x) || !aligned16(Wg)) return DMOE_EUNSUPPORTED;
-  GateArgs a{x, Wg, bg, alive, idx, w, g, scores, (int)s.T, (int)s.D, s.d, s.M, s.k, (int)s.dM};
-  const dim3 grid((unsigned)((s.T + GATE_TB - 1) / GATE_TB));
-  const size_t lds = gate_lds_bytes((int)s.dM);
+  GateArgs a{x, Wg, bg, alive, idx, w, g, scores, (int)s.T, (int)s.D, s.d, s.M, s.k, (int)s.dM, (int)s.N};
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (s.dtype == DMOE_BF16)
-    hipLaunchKernelGGL(gate_topk_kernel<bf16>, grid, dim3(GATE_NT), lds, st, a);
-  else
+  if (s.dtype == DMOE_BF16) {
+    // error factor of the MFMA scores (see select_token_cert)
+    const double u = 1.0 / 8388608.0;
+    const double g64 = 64 * u / (1 - 64 * u) + (s.D / 64 + 8) * 2.220446049250313e-16;
+    const double gD = (double)s.D * u / (1 - (double)s.D * u);
+    GateMfmaArgs ga{a, s.flags, (float)(g64 / (1 - gD) * 1.0001)};
+    const size_t lds = gate_mfma_lds_bytes((int)s.dM);
+    static bool attr = false;
+    if (!attr) {
+      (void)hipFuncSetAttribute((const void*)gate_topk_mfma, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)gate_mfma_lds_bytes(DM_MAX));
+      (void)hipGetLastError();
+      attr = true;
+    }
+    const dim3 grid((unsigned)((s.T + GM_TOK - 1) / GM_TOK));
+    hipLaunchKernelGGL(gate_topk_mfma, grid, dim3(GM_NT), lds, st, ga);
+  } else {
+    const dim3 grid((unsigned)((s.T + GATE_TB - 1) / GATE_TB));
+    const size_t lds = gate_lds_bytes((int)s.dM);
     hipLaunchKernelGGL(gate_topk_kernel<float>, grid, dim3(GATE_NT), lds, st, a);
+  }
   return launch_status();
 }
 

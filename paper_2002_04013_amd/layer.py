@@ -13,8 +13,8 @@ class DMoELayer:
     """Device buffers for one layer shape; parameters are passed per call."""
 
     def __init__(self, T, D, H, d, M, k, dtype="bf16", act="gelu", device="cuda",
-                 dh_aliases_h=False):
-        self.dims = abi.make_dims(T, D, H, d, M, k, dtype, act)
+                 dh_aliases_h=False, flags=0):
+        self.dims = abi.make_dims(T, D, H, d, M, k, dtype, act, flags)
         self.T, self.D, self.H, self.d, self.M, self.k = T, D, H, d, M, k
         self.N = M ** d
         self.P = T * k

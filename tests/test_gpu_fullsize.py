@@ -19,7 +19,7 @@ import pytest
 import torch
 
 import oracle as O
-from parity_util import RTOL, assert_close, say
+from parity_util import RTOL, assert_close, check_gate, say
 from workloads import get_workload, make_alive, make_dy, make_experts, make_gate, make_x
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
@@ -66,10 +66,15 @@ def test_fullsize_parity(name):
         idx, _ = O.topk_product_key(S32, wl.d, wl.M, wl.k)
     g = O.chosen_totals(S, idx, wl.d, wl.M)
     w = O.mixture_weights(g, idx, alive_h)
-    sc = O.to64(L.scores)
-    assert np.all(np.abs(sc - S) <= np.abs(S) * 2.0 ** -23 + 1e-30), "scores"
+    check_gate(wl, L.scores, L.w, None, S, w, g, x64, Wg64)
     np.testing.assert_array_equal(L.idx.cpu().numpy(), idx, "idx")
-    np.testing.assert_allclose(L.w.cpu().numpy(), w, rtol=1e-6, atol=1e-6, err_msg="w")
+    # the exact-accumulation path gives the same routing, bit for bit
+    from paper_2002_04013_amd import abi
+    idx2 = torch.empty_like(L.idx)
+    w2 = torch.empty_like(L.w)
+    abi.dmoe_gate_topk(abi.make_dims(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act,
+                                     abi.DMOE_FLAG_GATE_EXACT), x, Wg, bg, alive, idx2, w2, None, None, L.ws)
+    assert torch.equal(idx2, L.idx), "exact-path routing differs"
     counts, offsets, row_token, pos = O.dispatch(idx, alive_h, wl.N)
     np.testing.assert_array_equal(L.counts.cpu().numpy(), counts, "counts")
     np.testing.assert_array_equal(L.offsets.cpu().numpy(), offsets, "offsets")

@@ -141,3 +141,37 @@ def test_token_permutation_equivariance():
     assert torch.equal(b["idx"], a["idx"][perm])
     assert torch.equal(b["y"], a["y"][perm])
     assert torch.equal(b["dx"], a["dx"][perm])
+
+
+def test_gate_exact_flag_same_routing():
+    """DMOE_FLAG_GATE_EXACT computes every token's scores with exact fp64 accumulation
+    (the fallback path of the certified MFMA gate): same TopK, bit for bit."""
+    from paper_2002_04013_amd.abi import DMOE_FLAG_GATE_EXACT
+    wl = CASES["bf16_skew"]
+    say("[parity] exact-gate flag")
+    inp = make_inputs(wl, "cpu")
+    a = gpu_run(wl, inp, backward=False)
+    b = gpu_run(wl, inp, backward=False, flags=DMOE_FLAG_GATE_EXACT)
+    assert torch.equal(a["idx"], b["idx"])
+    fwd, _ = oracle_run(wl, inp, backward=False)
+    np.testing.assert_array_equal(b["idx"].numpy(), fwd["idx"])
+    S = fwd["S"]   # exact path: one fp32 rounding of the fp64-accumulated score
+    assert np.all(np.abs(b["scores"].double().numpy() - S) <= np.abs(S) * 2.0 ** -23 + 1e-30)
+
+
+def test_gate_exact_ties_fall_back():
+    """Duplicated gate rows make exactly tied scores and totals: no certificate is
+    possible, every affected token takes the exact path and ties go to the lower
+    flat index, as in the oracle."""
+    wl = Workload("ties", 24, T=512, D=128, H=128, d=2, M=8, k=4, dtype="bf16", act="gelu", p_alive=0.9)
+    say("[parity] exact ties in the gate")
+    inp = make_inputs(wl, "cpu")
+    Wg, bg = inp["Wg"].clone(), inp["bg"].clone()
+    for i in range(wl.d):          # rows u and u+1 equal in every dimension, for even u
+        for u in range(0, wl.M, 2):
+            Wg[i * wl.M + u + 1] = Wg[i * wl.M + u]
+            bg[i * wl.M + u + 1] = bg[i * wl.M + u]
+    inp["Wg"], inp["bg"] = Wg, bg
+    gpu = gpu_run(wl, inp)
+    fwd, bwd = oracle_run(wl, inp)
+    compare(wl, inp, gpu, fwd, bwd)
