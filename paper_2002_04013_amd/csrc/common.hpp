@@ -24,13 +24,16 @@ constexpr int WAVE = 64;
 
 __device__ __forceinline__ float bf2f(bf16 v) { return __uint_as_float((uint32_t)v << 16); }
 
-// fp32 -> bf16, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ bf16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16)(u >> 16);
+// fp32 -> bf16, round to nearest even, NaN stays NaN: the gfx950 packed conversion
+// v_cvt_pk_bf16_f32 (bit-identical, over every fp32 input, to rounding the bit
+// pattern by adding 0x7fff plus the lowest kept bit and quieting NaNs).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
+__device__ __forceinline__ bf16 f2bf(float f) { return (bf16)(f2bf2(f, 0.f) & 0xffffu); }
 
 template <typename E> __device__ __forceinline__ float ldf(const E* p);
 template <> __device__ __forceinline__ float ldf<float>(const float* p) { return *p; }
@@ -66,7 +69,7 @@ template <> struct Vec<bf16> {
   __device__ static uint4 pack(const float* f) {
     uint32_t w[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(f[2 * i]) | ((uint32_t)f2bf(f[2 * i + 1]) << 16);
+    for (int i = 0; i < 4; ++i) w[i] = f2bf2(f[2 * i], f[2 * i + 1]);
     return make_uint4(w[0], w[1], w[2], w[3]);
   }
 };

@@ -148,13 +148,20 @@ struct TileT {
 
 // Tile lookup: expert e owning global tile L; expert e's tiles start at
 // tprefix[e] * scale (tprefix is non-decreasing).
-__device__ __forceinline__ int find_group(const int32_t* tprefix, int scale, int groups, int L) {
-  int lo = 0, hi = groups;          // invariant: tprefix[lo]*scale <= L < tprefix[hi]*scale
+__device__ __forceinline__ int find_group(const int32_t* tprefix, int scale, int groups, int L, int lo = 0) {
+  int hi = groups;                  // invariant: tprefix[lo]*scale <= L < tprefix[hi]*scale
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
     if (tprefix[mid] * scale <= L) lo = mid; else hi = mid;
   }
   return lo;
+}
+// Same, for a tile index that is not below the one whose group was `hint`: a block
+// walks its tiles in increasing order, so the group is usually `hint` itself (one
+// load) or found by searching only above it.
+__device__ __forceinline__ int find_group_from(const int32_t* tprefix, int scale, int groups, int L, int hint) {
+  if (tprefix[hint + 1] * scale > L) return hint;
+  return find_group(tprefix, scale, groups, L, hint + 1);
 }
 
 template <typename E, int GM, bool B_KC, int EPI, int BM, int BN, int BK, int WM, int WN>

@@ -142,26 +142,57 @@ struct NcTile {
   }
 };
 
+// Runtime-selected s_waitcnt vmcnt(n) for n in [0, 63] (n is wave-uniform).
+__device__ __forceinline__ void wait_vmcnt_rt(int n) {
+  if (n >= 48) { if (n >= 56) wait_vmcnt<56>(); else wait_vmcnt<48>(); }
+  else if (n >= 32) { if (n >= 40) wait_vmcnt<40>(); else wait_vmcnt<32>(); }
+  else if (n >= 16) { if (n >= 24) wait_vmcnt<24>(); else wait_vmcnt<16>(); }
+  else if (n >= 12) wait_vmcnt<12>();
+  else if (n >= 8) wait_vmcnt<8>();
+  else if (n >= 4) wait_vmcnt<4>();
+  else wait_vmcnt<0>();
+}
+
+// Schedule of one tile, per wave:
+//   * the prologue issues every stage of the LDS ring (the ring is free once the
+//     previous tile's reads are done), before the previous tile's epilogue;
+//   * stage kt is consumed in BK/16 MFMA steps; the fragments of step kk+1 are read
+//     while the MFMAs of step kk run, and in the last step the wave waits for stage
+//     kt+1, passes the barrier, refills the ring slot of stage kt with stage
+//     kt+STAGES and reads the first fragments of stage kt+1, all before issuing the
+//     last MFMAs of stage kt, so no LDS latency is exposed at stage boundaries;
+//   * vector-memory operations (loads, stores, direct-to-LDS loads) retire from the
+//     vmcnt counter in issue order on gfx9-family chips, so "stage s has landed" is
+//     vmcnt <= (operations issued after stage s).  The previous tile's epilogue stores
+//     follow the prologue stages; they are counted only when that tile was full
+//     (exact count known), otherwise the wait also covers them.
+// Rows of a tile are split in 32-row blocks; block b belongs to wave row wm = b % WM
+// as its block j = b / WM, so a partly filled tile (the last m-tile of an expert)
+// spreads its live blocks over all wave rows and SIMDs.  Each wave runs a loop
+// specialised for its number of live blocks, so the loop body has no branches.
 template <int GM, bool A_T, bool B_T, int EPI, int BM, int BN, int WM, int WN, int STAGES, int SW, int BK>
 __global__ void __launch_bounds__(64 * WM * WN)
 grouped_gemm2(GemmArgs<bf16> p) {
   constexpr int NW = WM * WN, NT = 64 * NW;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int KK = BK / 16;
   using TA = typename std::conditional<A_T, NcTile<BM, NW, BK>, KcTile<BM, NW, SW, BK>>::type;
   using TB = typename std::conditional<B_T, NcTile<BN, NW, BK>, KcTile<BN, NW, SW, BK>>::type;
   constexpr int ABYTES = TA::BYTES, SBYTES = TA::BYTES + TB::BYTES;
-  static_assert(TM >= 1 && TN >= 1, "tile");
+  constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave
+  // store instructions of a full tile's epilogue, per wave
+  constexpr int SFULL = TM * TN * 4 * (EPI == EPI_BIAS_ACT ? 2 : 1);
+  static_assert(TM >= 1 && TM <= 4 && TN >= 1, "tile");
+  static_assert(KK % 2 == 0, "fragment slots alternate over an even number of steps");
   static_assert(TA::INSTR % NW == 0 && TB::INSTR % NW == 0, "equal load counts per wave");
   static_assert(GM == GROUP_M || (A_T && B_T), "GROUP_K takes both operands stored per token");
+  static_assert(STAGES * LPS <= 63, "vmcnt range");
 
   extern __shared__ __align__(1024) char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // Waves go to the 4 SIMDs round-robin; with wm = wave / WN the two waves sharing a
-  // SIMD cover different row ranges, so in a partly filled m-tile (the last tile of
-  // an expert) the wave with no rows left hands its SIMD's matrix core to the other.
   const int wm = wave / WN, wn = wave % WN;
 
   const int total = p.tprefix[p.groups] * p.tscale;
@@ -182,9 +213,11 @@ grouped_gemm2(GemmArgs<bf16> p) {
     const bf16* Ab;
     const bf16* Bb;
   };
+  int ehint = 0;                   // group of the previous tile of this block
   auto setup = [&](int Lt) {
     TileC t;
-    t.e = find_group(p.tprefix, p.tscale, p.groups, Lt);
+    t.e = find_group_from(p.tprefix, p.tscale, p.groups, Lt, ehint);
+    ehint = t.e;
     const int q = Lt - p.tprefix[t.e] * p.tscale;
     t.off = p.offsets[t.e];
     const int cnt = p.offsets[t.e + 1] - t.off;
@@ -222,27 +255,37 @@ grouped_gemm2(GemmArgs<bf16> p) {
   };
   auto prologue = [&](const TileC& t) {
 #pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
+    for (int s = 0; s < STAGES; ++s)
       if (s < t.nk) issue(t, s);
   };
-  constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave
+  // stage s of tile t has landed in this wave's view; `after` = load stages issued after it
+  auto wait_stage = [&](int after, int extra) { wait_vmcnt_rt(after * LPS + extra > 63 ? 63 : after * LPS + extra); };
+  // GROUP_K: zero the k rows of stage s past the expert's tokens, once every wave's loads landed
+  auto fix_tail = [&](const TileC& t, int s) {
+    if constexpr (GM == GROUP_K) {
+      const int kv = t.kvalid - s * BK;
+      if (kv < BK) {
+        char* buf = smem + (s % STAGES) * SBYTES;
+        block_sync_lds();
+        TA::zero_tail(buf, kv, tid, NT);
+        TB::zero_tail(buf + ABYTES, kv, tid, NT);
+      }
+    }
+  };
 
-  // The first stages of a tile are issued before the previous tile's epilogue, so
-  // their latency overlaps its arithmetic and stores.
   TileC nxt{};
   if (L < Lend) {
-    wait_vmcnt<0>();
     nxt = setup(L);
     prologue(nxt);
   }
+  int prev_stores = 0;            // exact store count of the previous epilogue, 0 if unknown
   for (; L < Lend; L += Lstep) {
     const TileC t = nxt;
     const int e = t.e, off = t.off, m0 = t.m0, n0 = t.n0, mvalid = t.mvalid, nvalid = t.nvalid;
-    const int kvalid = t.kvalid, nk = t.nk;
-    // 32-row blocks of this wave that hold rows of the tile (wave-uniform)
-    bool jlive[TM];
-#pragma unroll
-    for (int j = 0; j < TM; ++j) jlive[j] = wm * WTM + j * 32 < mvalid;
+    const int nk = t.nk;
+    const int nblk = (mvalid + 31) / 32;                 // live 32-row blocks of the tile
+    int nl = (nblk - wm + WM - 1) / WM;                  // of them, this wave's (a prefix of j)
+    nl = nl < 0 ? 0 : (nl > TM ? TM : nl);
 
     f32x16_t acc[TN][TM];
 #pragma unroll
@@ -252,94 +295,112 @@ grouped_gemm2(GemmArgs<bf16> p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    for (int kt = 0; kt < nk; ++kt) {
-      // stage kt must have landed.  At kt = 0 everything outstanding is drained: the
-      // prologue of this tile and the previous tile's epilogue stores.
-      const int ahead = nk - 1 - kt;                  // stages issued after kt (capped below)
-      if (kt == 0) {
-        wait_vmcnt<0>();
-      } else if constexpr (STAGES >= 4) {
-        if (ahead >= 2) wait_vmcnt<2 * LPS>(); else if (ahead == 1) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
-      } else if constexpr (STAGES == 3) {
-        if (ahead >= 1) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      char* buf = smem + (kt % STAGES) * SBYTES;
-      if constexpr (GM == GROUP_K) {
-        const int kv = kvalid - kt * BK;
-        if (kv < BK) {                                // zero the k rows past the expert's tokens
-          block_sync_lds();                            // (after every wave's loads of this stage landed)
-          TA::zero_tail(buf, kv, tid, NT);
-          TB::zero_tail(buf + ABYTES, kv, tid, NT);
-        }
-      }
-      block_sync_lds();
-      if (kt + STAGES - 1 < nk) issue(t, kt + STAGES - 1);
-      const char* as = buf;
-      const char* bs = buf + ABYTES;
-      // Fragments are double-buffered across the 16-deep k steps: the reads for step
-      // kk+1 are issued before the MFMAs of step kk, and the scheduler is asked to
-      // interleave the two so LDS latency hides behind matrix work.
-      constexpr int KK = BK / 16;
-      constexpr int NDS = (A_T ? 2 : 1) * TM + (B_T ? 2 : 1) * TN;   // LDS reads per step
+    auto mainloop = [&](auto NLc) {
+      constexpr int NL = decltype(NLc)::value;
+      constexpr int NDS = (A_T ? 2 : 1) * NL + (B_T ? 2 : 1) * TN;   // LDS reads per step
       bf16x8_t fa[2][TM], fb[2][TN];
-      auto ldfrag = [&](int kk, bf16x8_t* A_, bf16x8_t* B_) {
+      auto ldfrag = [&](const char* buf, int kk, int slot) {
+        if constexpr (NL == 0) return;             // no rows: nothing to multiply
+        const char* as = buf;
+        const char* bs = buf + ABYTES;
 #pragma unroll
-        for (int j = 0; j < TM; ++j) {
-          if (!jlive[j]) continue;
-          if constexpr (A_T) A_[j] = TA::frag(as, wm * WTM + j * 32, kk * 16, lane);
-          else A_[j] = TA::frag(as, wm * WTM + j * 32, kk * 2, lane);
+        for (int j = 0; j < NL; ++j) {
+          const int r0 = (j * WM + wm) * 32;
+          if constexpr (A_T) fa[slot][j] = TA::frag(as, r0, kk * 16, lane);
+          else fa[slot][j] = TA::frag(as, r0, kk * 2, lane);
         }
 #pragma unroll
         for (int i = 0; i < TN; ++i) {
-          if constexpr (B_T) B_[i] = TB::frag(bs, wn * WTN + i * 32, kk * 16, lane);
-          else B_[i] = TB::frag(bs, wn * WTN + i * 32, kk * 2, lane);
+          if constexpr (B_T) fb[slot][i] = TB::frag(bs, wn * WTN + i * 32, kk * 16, lane);
+          else fb[slot][i] = TB::frag(bs, wn * WTN + i * 32, kk * 2, lane);
         }
       };
-      ldfrag(0, fa[0], fb[0]);
+      auto mm = [&](int slot) {
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const int cb = kk & 1;
-        if (kk + 1 < KK) ldfrag(kk + 1, fa[cb ^ 1], fb[cb ^ 1]);
-#pragma unroll
-        for (int j = 0; j < TM; ++j) {
-          if (!jlive[j]) continue;
+        for (int j = 0; j < NL; ++j)
 #pragma unroll
           for (int i = 0; i < TN; ++i)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cb][i], fa[cb][j], acc[i][j], 0, 0, 0);
-        }
-        if (kk + 1 < KK) {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][i], fa[slot][j], acc[i][j], 0, 0, 0);
+      };
+      auto interleave = [&]() {
 #pragma unroll
-          for (int q = 0; q < TM * TN; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // one MFMA
-            if (q < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-          }
+        for (int q = 0; q < NL * TN; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // one MFMA
+          if (q < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
         }
+      };
+      // stage 0: issued in the prologue, followed by the load stages 1.. and the
+      // previous tile's epilogue stores
+      {
+        const int issued = nk < STAGES ? nk : STAGES;
+        wait_stage(issued - 1, prev_stores);
+        fix_tail(t, 0);
+        block_sync_lds();
+        ldfrag(smem, 0, 0);
       }
-    }
+      // every stage but the last: the last MFMA step also moves on to the next stage
+      for (int kt = 0; kt + 1 < nk; ++kt) {
+        const char* cur = smem + (kt % STAGES) * SBYTES;
+#pragma unroll
+        for (int kk = 0; kk + 1 < KK; ++kk) {
+          ldfrag(cur, kk + 1, (kk & 1) ^ 1);
+          mm(kk & 1);
+          interleave();
+        }
+        // stages issued after kt+1: up to kt+STAGES-1, capped by the last stage; the
+        // previous epilogue's stores come after the prologue stages 0..STAGES-1
+        const int last = kt + STAGES - 1 < nk - 1 ? kt + STAGES - 1 : nk - 1;
+        wait_stage(last - (kt + 1), kt + 1 < STAGES ? prev_stores : 0);
+        fix_tail(t, kt + 1);
+        block_sync_lds();               // every wave is done with slot kt and sees stage kt+1
+        if (kt + STAGES < nk) issue(t, kt + STAGES);
+        ldfrag(smem + ((kt + 1) % STAGES) * SBYTES, 0, 0);
+        mm(1);
+        interleave();
+      }
+      {
+        const char* cur = smem + ((nk - 1) % STAGES) * SBYTES;
+#pragma unroll
+        for (int kk = 0; kk + 1 < KK; ++kk) {
+          ldfrag(cur, kk + 1, (kk & 1) ^ 1);
+          mm(kk & 1);
+          interleave();
+        }
+        mm(1);
+      }
+    };
+    if (nl == TM) mainloop(std::integral_constant<int, TM>{});
+    else if (TM >= 2 && nl == 1) mainloop(std::integral_constant<int, 1>{});
+    else if (TM >= 3 && nl == 2) mainloop(std::integral_constant<int, (TM >= 3 ? 2 : 1)>{});
+    else if (TM >= 4 && nl == 3) mainloop(std::integral_constant<int, (TM >= 4 ? 3 : 1)>{});
+    else mainloop(std::integral_constant<int, 0>{});
+
     block_sync_lds();      // every wave is done with the ring before the next tile's loads
     if (L + Lstep < Lend) {
       nxt = setup(L + Lstep);
       prologue(nxt);
     }
 
-    // epilogue (same accumulator layout as grouped_gemm)
+    // epilogue (same accumulator layout as grouped_gemm); stores issued by this wave
+    // number SFULL exactly when every row and column of its part of the tile is valid
+    const bool full = nl == TM && mvalid >= BM && nvalid >= BN;
+    prev_stores = full ? SFULL : 0;
     const int l32 = lane & 31, lhi = lane >> 5;
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
-      const int ml = wm * WTM + j * 32 + l32;
-      if (ml >= mvalid) continue;
+      const int ml = (j * WM + wm) * 32 + l32;
+      if (j >= nl) continue;
       int64_t crow;
       if constexpr (GM == GROUP_M) crow = (int64_t)(off + m0 + ml) * p.ldc;
       else crow = (int64_t)e * p.c_gstride + (int64_t)(m0 + ml) * p.ldc;
+      const bool mok = ml < mvalid;
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int nl = wn * WTN + i * 32 + 8 * g + 4 * lhi;
-          if (nl >= nvalid) continue;
-          const int n = n0 + nl;
+          const int nl_ = wn * WTN + i * 32 + 8 * g + 4 * lhi;
+          if (!mok || nl_ >= nvalid) continue;
+          const int n = n0 + nl_;
           float v[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * g + r];
@@ -357,15 +418,13 @@ grouped_gemm2(GemmArgs<bf16> p) {
             *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) = make_float4(v[0], v[1], v[2], v[3]);
           } else {
             bf16* cp = reinterpret_cast<bf16*>(p.C) + crow + n;
-            *reinterpret_cast<uint2*>(cp) = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
-                                                       (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+            *reinterpret_cast<uint2*>(cp) = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
             if constexpr (EPI == EPI_BIAS_ACT) {
               float a[4];
 #pragma unroll
               for (int r = 0; r < 4; ++r) a[r] = act_fwd(v[r], p.act);
               bf16* ap = reinterpret_cast<bf16*>(p.C2) + crow + n;
-              *reinterpret_cast<uint2*>(ap) = make_uint2((uint32_t)f2bf(a[0]) | ((uint32_t)f2bf(a[1]) << 16),
-                                                         (uint32_t)f2bf(a[2]) | ((uint32_t)f2bf(a[3]) << 16));
+              *reinterpret_cast<uint2*>(ap) = make_uint2(f2bf2(a[0], a[1]), f2bf2(a[2], a[3]));
             }
           }
         }
