@@ -376,16 +376,41 @@ grouped_gemm2(GemmArgs<bf16> p) {
     else mainloop(std::integral_constant<int, 0>{});
 
     block_sync_lds();      // every wave is done with the ring before the next tile's loads
-    if (L + Lstep < Lend) {
+
+    // Epilogue operands read from memory are loaded before the next tile's loads where
+    // registers allow: vector-memory operations retire in issue order, so a load issued
+    // after the prologue waits for it.  The bias (one row, TN x 4 values) is loaded
+    // first.  The activation derivative reads a whole tile of h, too large to hold
+    // next to the accumulators; its loads follow only the first stage of the next tile,
+    // and the remaining stages are issued after the epilogue.
+    const int l32 = lane & 31, lhi = lane >> 5;
+    constexpr bool HAS_BIAS = EPI == EPI_BIAS || EPI == EPI_BIAS_ACT;
+    constexpr bool HAS_AUX = EPI == EPI_DACT;
+    constexpr int PRE = HAS_AUX ? 1 : STAGES;       // prologue stages issued before the epilogue
+    uint2 bias_v[HAS_BIAS ? TN : 1][4];
+    if constexpr (HAS_BIAS) {
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int nl_ = wn * WTN + i * 32 + 8 * g + 4 * lhi;
+          const int n = n0 + (nl_ < nvalid ? nl_ : 0);
+          bias_v[i][g] = *reinterpret_cast<const uint2*>(p.bias + (int64_t)e * p.bias_gstride + n);
+        }
+    }
+
+    const bool more = L + Lstep < Lend;
+    if (more) {
       nxt = setup(L + Lstep);
-      prologue(nxt);
+#pragma unroll
+      for (int st = 0; st < PRE; ++st)
+        if (st < nxt.nk) issue(nxt, st);
     }
 
     // epilogue (same accumulator layout as grouped_gemm); stores issued by this wave
     // number SFULL exactly when every row and column of its part of the tile is valid
     const bool full = nl == TM && mvalid >= BM && nvalid >= BN;
     prev_stores = full ? SFULL : 0;
-    const int l32 = lane & 31, lhi = lane >> 5;
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       const int ml = (j * WM + wm) * 32 + l32;
@@ -394,6 +419,19 @@ grouped_gemm2(GemmArgs<bf16> p) {
       if constexpr (GM == GROUP_M) crow = (int64_t)(off + m0 + ml) * p.ldc;
       else crow = (int64_t)e * p.c_gstride + (int64_t)(m0 + ml) * p.ldc;
       const bool mok = ml < mvalid;
+      // h of this 32-row block for the activation derivative, all loaded before the
+      // block's first store (a load issued after a store also waits for the store)
+      uint2 aux_v[HAS_AUX ? TN : 1][4];
+      if constexpr (HAS_AUX) {
+        const int64_t arow = (int64_t)(off + m0 + (mok ? ml : 0)) * p.ldc;
+#pragma unroll
+        for (int i = 0; i < TN; ++i)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int nl_ = wn * WTN + i * 32 + 8 * g + 4 * lhi;
+            aux_v[i][g] = *reinterpret_cast<const uint2*>(p.aux + arow + n0 + (nl_ < nvalid ? nl_ : 0));
+          }
+      }
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
 #pragma unroll
@@ -404,15 +442,17 @@ grouped_gemm2(GemmArgs<bf16> p) {
           float v[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * g + r];
-          if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_ACT) {
-            const bf16* bp = p.bias + (int64_t)e * p.bias_gstride + n;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] += bf2f(bp[r]);
+          if constexpr (HAS_BIAS) {
+            const uint2 b = bias_v[i][g];
+            v[0] += __uint_as_float(b.x << 16); v[1] += __uint_as_float(b.x & 0xffff0000u);
+            v[2] += __uint_as_float(b.y << 16); v[3] += __uint_as_float(b.y & 0xffff0000u);
           }
-          if constexpr (EPI == EPI_DACT) {
-            const bf16* hp = p.aux + crow + n;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] *= act_bwd(bf2f(hp[r]), p.act);
+          if constexpr (HAS_AUX) {
+            const uint2 hv = aux_v[i][g];
+            v[0] *= act_bwd_fast(__uint_as_float(hv.x << 16), p.act);
+            v[1] *= act_bwd_fast(__uint_as_float(hv.x & 0xffff0000u), p.act);
+            v[2] *= act_bwd_fast(__uint_as_float(hv.y << 16), p.act);
+            v[3] *= act_bwd_fast(__uint_as_float(hv.y & 0xffff0000u), p.act);
           }
           if constexpr (EPI == EPI_F32) {
             *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) = make_float4(v[0], v[1], v[2], v[3]);
@@ -422,12 +462,21 @@ grouped_gemm2(GemmArgs<bf16> p) {
             if constexpr (EPI == EPI_BIAS_ACT) {
               float a[4];
 #pragma unroll
-              for (int r = 0; r < 4; ++r) a[r] = act_fwd(v[r], p.act);
+              for (int r = 0; r < 4; ++r) a[r] = act_fwd_fast(v[r], p.act);
               bf16* ap = reinterpret_cast<bf16*>(p.C2) + crow + n;
               *reinterpret_cast<uint2*>(ap) = make_uint2(f2bf2(a[0], a[1]), f2bf2(a[2], a[3]));
             }
           }
         }
+      }
+    }
+    if constexpr (PRE < STAGES) {
+      // stages issued after the epilogue: the stores are no longer the newest operations
+      prev_stores = 0;
+      if (more) {
+#pragma unroll
+        for (int st = PRE; st < STAGES; ++st)
+          if (st < nxt.nk) issue(nxt, st);
       }
     }
   }
