@@ -94,7 +94,8 @@ const char* dmoe_strerror(int code);
  * tie is recomputed with exact fp64 accumulation, so the selection equals the one
  * of the exact scores; the returned scores, g and w carry the (bounded) MFMA error.
  * fp32: exact fp64 accumulation for every token.
- * Uses workspace: no. */
+ * Uses workspace: bf16 yes (the queue of tokens to recompute; ws must not be NULL),
+ * fp32 no. */
 int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* Wg, const void* bg,
                    const uint8_t* alive, int32_t* idx, float* w, float* g, float* scores,
                    void* ws, void* stream);

@@ -58,6 +58,9 @@ Workspace workspace_layout(const Shape& s) {
   w.part_off = off;
   w.part_bytes = align256((size_t)w.gsplit * w.ds_ld * s.D * sizeof(float));
   off += w.part_bytes;
+  w.gq_off = off;
+  w.gq_bytes = align256((size_t)(GQ_HEAD + s.T) * sizeof(int32_t));
+  off += w.gq_bytes;
   w.total = off;
   return w;
 }

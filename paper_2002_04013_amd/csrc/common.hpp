@@ -147,6 +147,7 @@ struct Workspace {
   size_t tiles_off, tiles_bytes;   // grouped GEMM: tile prefix [N+1] + per-expert m-tiles
   size_t ds_off, ds_bytes;         // gate backward: dense ds (bf16 hi/lo or fp32)
   size_t part_off, part_bytes;     // gate backward: dWg partial sums per token split
+  size_t gq_off, gq_bytes;         // gate forward: [0] count, [GQ_HEAD + i] tokens to recompute
   size_t total;
   int64_t disp_blocks;             // dispatch blocks (pairs per block = DISP_CHUNK)
   int64_t gsplit, gsplit_tokens;   // gate backward token splits
@@ -154,6 +155,7 @@ struct Workspace {
 };
 
 constexpr int DISP_CHUNK = 1024;   // pairs per dispatch block
+constexpr int GQ_HEAD = 64;        // gate queue: the count sits on its own 256-byte line
 
 Workspace workspace_layout(const Shape& s);
 

@@ -76,15 +76,15 @@ def oracle_run(wl, inp, backward=True):
 def score_error_bound(x64, Wg64, dtype):
     """Per-score bound on |GPU score - exact score| before the final fp32 rounding.
     fp32 layers accumulate exactly (fp64); bf16 layers sum exact bf16 products in
-    fp32 chunks of 64 (MFMA) and add the chunks in fp64: the error is at most
-    (gamma_64 + (D/64 + 8) 2^-52) sum_k |x_k w_k|, gamma_n = n u/(1 - n u), u = 2^-23."""
+    fp32 chunks of 32 (MFMA) and add the chunks in fp64: the error is at most
+    (gamma_32 + (D/32 + 8) 2^-52) sum_k |x_k w_k|, gamma_n = n u/(1 - n u), u = 2^-23."""
     if dtype != "bf16":
         return np.zeros((x64.shape[0], Wg64.shape[0]))
     D = x64.shape[1]
     u = 2.0 ** -23
-    g64 = 64 * u / (1 - 64 * u) + (D // 64 + 8) * 2.0 ** -52
+    g32 = 32 * u / (1 - 32 * u) + (D // 32 + 8) * 2.0 ** -52
     A = np.abs(x64) @ np.abs(Wg64).T
-    return g64 * A * 1.001
+    return g32 * A * 1.001
 
 
 def check_gate(wl, gpu_scores, gpu_w, gpu_g, S, w_ref, g_ref, x64, Wg64):
