@@ -4,6 +4,7 @@
 
 #include "common.hpp"
 #include "gemm.hpp"
+#include "gemm2.hpp"
 
 namespace dmoe {
 
@@ -34,10 +35,11 @@ struct GateArgs {
 // is kept only if their totals are separated by more than 2E, E = d (delta_max +
 // amax 2^-23) with delta = gam * ab[c] the bound on the score's accumulation error;
 // the span must stay below 2^25.  Returns false (nothing written) otherwise.
-template <bool CERT>
-__device__ __forceinline__ bool select_token(const double* s64, const float* ab, const uint8_t* alive, int d, int M, int k,
-                             int N, float gam, int32_t* idx_out, float* w_out, float* g_out) {
-  constexpr int CAP = KMAX + 1;
+// CAP: list capacity, at least K1 (the callers pick 5 when K1 <= 5, else KMAX + 1).
+template <bool CERT, int CAP>
+__device__ __forceinline__ bool select_token_cap(const double* s64, const float* ab, const uint8_t* alive, int d,
+                                                 int M, int k, int N, float gam, int32_t* idx_out, float* w_out,
+                                                 float* g_out) {
   const int K1 = CERT && k < N ? k + 1 : k;
   const int L = K1 < M ? K1 : M;
   float lv[DMAX][CAP];
@@ -65,60 +67,85 @@ __device__ __forceinline__ bool select_token(const double* s64, const float* ab,
       }
     }
   }
+  // top K1 cells: fp64 total, flat index, and the grid indices packed 8 bits per dim
   double tv[CAP];
-  int tf[CAP];
+  int tf[CAP], tu[CAP];
 #pragma unroll
-  for (int p = 0; p < CAP; ++p) { tv[p] = -INFINITY; tf[p] = 0x7fffffff; }
-  auto insert = [&](double v, int f) {
+  for (int p = 0; p < CAP; ++p) { tv[p] = -INFINITY; tf[p] = 0x7fffffff; tu[p] = 0; }
+  auto insert = [&](double v, int f, int uu) {
 #pragma unroll
     for (int p = 0; p < CAP; ++p) {
       const bool sw = v > tv[p] || (v == tv[p] && f < tf[p]);
       const double ov = tv[p];
-      const int of = tf[p];
-      tv[p] = sw ? v : ov; tf[p] = sw ? f : of;
-      v = sw ? ov : v; f = sw ? of : f;
+      const int of = tf[p], ou = tu[p];
+      tv[p] = sw ? v : ov; tf[p] = sw ? f : of; tu[p] = sw ? uu : ou;
+      v = sw ? ov : v; f = sw ? of : f; uu = sw ? ou : uu;
     }
   };
   const bool narrow = !(amax > 0.f) || amax <= amin * (CERT ? 33554432.f : 67108864.f);   // 2^25 / 2^26
   if (CERT && !narrow) return false;
   if (narrow) {
-    int ncand = 1;
+    // odometer over the rank digits r_0 .. r_{d-1} (last digit fastest), visiting only
+    // the tuples with prod(r_i + 1) <= K1: a digit whose prefix product would exceed
+    // K1 carries into the previous digit at once
+    int r[DMAX];
 #pragma unroll
-    for (int i = 0; i < DMAX; ++i) if (i < d) ncand *= L;
-    for (int q = 0; q < ncand; ++q) {
-      int rem = q, prod = 1;
-      int r[DMAX];
+    for (int i = 0; i < DMAX; ++i) r[i] = 0;
+    for (int guard = 0; guard < 4096; ++guard) {
+      int prod = 1;
+#pragma unroll
+      for (int i = 0; i < DMAX; ++i) if (i < d) prod *= r[i] + 1;
+      if (prod <= K1) {
+        double tot = 0.0;
+        int flat = 0, uu = 0;
+#pragma unroll
+        for (int i = 0; i < DMAX; ++i) {
+          if (i < d) {
+            // element r[i] of the lists, by selects (the lists stay in registers)
+            float pv = lv[i][0];
+            int pi = li[i][0];
+#pragma unroll
+            for (int p = 1; p < CAP; ++p) { pv = r[i] == p ? lv[i][p] : pv; pi = r[i] == p ? li[i][p] : pi; }
+            tot += (double)pv;
+            flat = flat * M + pi;
+            uu |= pi << (8 * i);
+          }
+        }
+        insert(tot, flat, uu);
+      }
+      // next tuple: bump the last digit; a digit that reaches L, or makes the product
+      // exceed K1 (so every larger value of it does too), resets and carries
+      bool carry = true;
 #pragma unroll
       for (int i = DMAX - 1; i >= 0; --i) {
-        r[i] = 0;
-        if (i < d) { r[i] = rem % L; rem /= L; prod *= r[i] + 1; }
-      }
-      if (prod > K1) continue;
-      double tot = 0.0;
-      int flat = 0;
+        if (i < d && carry) {
+          r[i] += 1;
+          int pr = 1;
 #pragma unroll
-      for (int i = 0; i < DMAX; ++i) {
-        if (i < d) {
-          // element r[i] of the lists, by selects (the lists stay in registers)
-          float pv = lv[i][0];
-          int pi = li[i][0];
-#pragma unroll
-          for (int p = 1; p < CAP; ++p) { pv = r[i] == p ? lv[i][p] : pv; pi = r[i] == p ? li[i][p] : pi; }
-          tot += (double)pv;
-          flat = flat * M + pi;
+          for (int ii = 0; ii < DMAX; ++ii) if (ii < d) pr *= r[ii] + 1;
+          if (r[i] >= L || pr > K1) r[i] = 0;
+          else carry = false;
         }
       }
-      insert(tot, flat);
+      if (carry) break;                  // every digit wrapped: done
     }
   } else {
+    int u[DMAX];
+#pragma unroll
+    for (int i = 0; i < DMAX; ++i) u[i] = 0;
     for (int f = 0; f < N; ++f) {
       double tot = 0.0;
-      int rem = f, u[DMAX];
+      int uu = 0;
 #pragma unroll
-      for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < d) { u[i] = rem % M; rem /= M; } }
+      for (int i = 0; i < DMAX; ++i) if (i < d) { tot += (double)(float)s64[i * M + u[i]]; uu |= u[i] << (8 * i); }
+      insert(tot, f, uu);
 #pragma unroll
-      for (int i = 0; i < DMAX; ++i) if (i < d) tot += (double)(float)s64[i * M + u[i]];
-      insert(tot, f);
+      for (int i = DMAX - 1; i >= 0; --i) {        // next flat index: last dim fastest
+        if (i < d) {
+          if (++u[i] < M) break;
+          u[i] = 0;
+        }
+      }
     }
   }
   if constexpr (CERT) {
@@ -130,34 +157,33 @@ __device__ __forceinline__ bool select_token(const double* s64, const float* ab,
     if (!sep) return false;
   }
   // Eq. 1 weights from the fp64 totals of the chosen experts, over the alive ones
-  double gx[KMAX];
-  bool live[KMAX];
+  constexpr int KJ = CAP < KMAX ? CAP : KMAX;      // k <= K1 <= CAP
+  double gx[KJ];
+  bool live[KJ];
+#pragma unroll
+  for (int j = 0; j < KJ; ++j) live[j] = j < k && (alive == nullptr || alive[tf[j]] != 0);
   double m = -1.0e308;
   bool any = false;
 #pragma unroll
-  for (int j = 0; j < KMAX; ++j) {
-    gx[j] = 0.0; live[j] = false;
+  for (int j = 0; j < KJ; ++j) {
+    gx[j] = 0.0;
     if (j < k) {
-      int rem = tf[j], u[DMAX];
-#pragma unroll
-      for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < d) { u[i] = rem % M; rem /= M; } }
       double t = 0.0;
 #pragma unroll
-      for (int i = 0; i < DMAX; ++i) if (i < d) t += s64[i * M + u[i]];
+      for (int i = 0; i < DMAX; ++i) if (i < d) t += s64[i * M + ((tu[j] >> (8 * i)) & 0xff)];
       gx[j] = t;
-      live[j] = alive == nullptr || alive[tf[j]] != 0;
       if (live[j]) { any = true; m = t > m ? t : m; }
     }
   }
-  float ex[KMAX];
+  float ex[KJ];
   float sum = 0.f;
 #pragma unroll
-  for (int j = 0; j < KMAX; ++j) {
-    ex[j] = j < k && live[j] ? expf((float)(gx[j] - m)) : 0.f;
+  for (int j = 0; j < KJ; ++j) {
+    ex[j] = live[j] ? expf((float)(gx[j] - m)) : 0.f;
     sum += ex[j];
   }
 #pragma unroll
-  for (int j = 0; j < KMAX; ++j) {
+  for (int j = 0; j < KJ; ++j) {
     if (j < k) {
       idx_out[j] = tf[j];
       w_out[j] = any ? ex[j] / sum : 0.f;
@@ -165,6 +191,14 @@ __device__ __forceinline__ bool select_token(const double* s64, const float* ab,
     }
   }
   return true;
+}
+
+template <bool CERT>
+__device__ __forceinline__ bool select_token(const double* s64, const float* ab, const uint8_t* alive, int d, int M,
+                                             int k, int N, float gam, int32_t* idx_out, float* w_out, float* g_out) {
+  const int K1 = CERT && k < N ? k + 1 : k;
+  if (K1 <= 5) return select_token_cap<CERT, 5>(s64, ab, alive, d, M, k, N, gam, idx_out, w_out, g_out);
+  return select_token_cap<CERT, KMAX + 1>(s64, ab, alive, d, M, k, N, gam, idx_out, w_out, g_out);
 }
 
 template <typename E>
@@ -255,9 +289,11 @@ __global__ void __launch_bounds__(GATE_NT) gate_topk_kernel(GateArgs a) {
 // the same order; such tokens are certified.  The others are appended to a device
 // queue and recomputed with exact fp64 accumulation by gate_exact_kernel.
 
-constexpr int GM_TOK = 32;        // tokens per block
-constexpr int GM_NT = 256;        // 4 waves, each a quarter of the d_model contraction
-constexpr int GX_NT = 256;        // exact recomputation: threads per token
+constexpr int GM_TOK = 32;        // tokens per block (one MFMA row block)
+constexpr int GM_KW = 2;          // waves per block, each a share of the d_model groups
+constexpr int GM_NT = 64 * GM_KW;
+constexpr int GM_RING = 4;        // x groups (32 tokens x 64 d_model, 4 KB) in flight per wave
+constexpr int GX_NT = 512;        // exact recomputation: threads per token
 
 struct GateMfmaArgs {
   GateArgs a;
@@ -266,113 +302,153 @@ struct GateMfmaArgs {
   int32_t* queue;                  // [0] count, [GQ_HEAD + i] token ids
 };
 
+__device__ __forceinline__ void g2l16(const void* g, void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void*)g,
+                                   (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0, 0);
+}
+
+// A block of GM_KW waves scores 32 tokens against all d*M gate columns; wave w takes
+// the d_model groups w, w + GM_KW, ... (groups of 64 values).  x and Wg stream
+// through a per-wave LDS ring of GM_RING groups (direct global->LDS loads, 8 rows x
+// 128 bytes per instruction, 16-byte chunks XOR-swizzled by row): a slot holds 32
+// token rows, then 32*CB gate-column rows.  Within a group, lane half h holds
+// d_model offsets 32h .. 32h+31 and MFMA chunk j takes 32h+8j .. 32h+8j+7 from both
+// operands (the contraction order is permuted identically for x and Wg).  The
+// waves' fp64 partial sums are added in wave order in LDS, then one lane per token
+// selects.
+template <int CB>                      // 32-column blocks of the d*M gate columns
 __global__ void __launch_bounds__(GM_NT) gate_topk_mfma(GateMfmaArgs ga) {
   const GateArgs& a = ga.a;
-  extern __shared__ __align__(16) unsigned char sm[];
+  extern __shared__ __align__(1024) unsigned char sm[];
+  constexpr int SLOT = 4096 * (1 + CB);          // bytes per ring slot
+  constexpr int LPG = 4 * (1 + CB);              // load instructions per group
   const int dM = a.dM;
-  // per-token rows are padded to an odd number of 4- or 8-byte words, so that the 32
-  // tokens of a half-wave fall on distinct LDS banks
-  const int SLD = dM + 1;
-  double* s64 = reinterpret_cast<double*>(sm);                               // [TOK][SLD]
-  float* ab = reinterpret_cast<float*>(s64 + GM_TOK * SLD);                  // [TOK][SLD]
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int t0 = blockIdx.x * GM_TOK;
   const bool exact_all = (ga.flags & DMOE_FLAG_GATE_EXACT) != 0;
   if (exact_all) {                       // every token goes to the exact path
-    if (tid < GM_TOK && t0 + tid < a.T) ga.queue[GQ_HEAD + atomicAdd(ga.queue, 1)] = t0 + tid;
+    if (threadIdx.x < GM_TOK && t0 + threadIdx.x < a.T)
+      ga.queue[GQ_HEAD + atomicAdd(ga.queue, 1)] = t0 + threadIdx.x;
     return;
   }
   const bf16* x = reinterpret_cast<const bf16*>(a.x);
   const bf16* W = reinterpret_cast<const bf16*>(a.Wg);
   const bf16* bg = reinterpret_cast<const bf16*>(a.bg);
-  const int tok = lane & 31;                                   // token of this lane within the block
-  const int trow = min(t0 + tok, a.T - 1);
-  const int half = lane >> 5;
-  const int CB = (dM + 31) / 32;
-  // d_model is cut in groups of 64; wave w takes groups w, w+4, ...  Within a group,
-  // lane half h holds k = 32h .. 32h+31, four 16-byte loads issued back to back (whole
-  // 128-byte lines per row), and MFMA chunk j takes its 8 elements 32h+8j .. 32h+8j+7
-  // from both x and Wg, so every product x_k w_k appears once (contraction order permuted).
+  const int tok = lane & 31, half = lane >> 5;
   const int NG = a.D / 64;
-  const int ng = NG > wave ? (NG - wave + 3) / 4 : 0;         // groups of this wave
-  for (int cb = 0; cb < CB; ++cb) {
-    const int col = min(cb * 32 + (lane & 31), dM - 1);
-    const bf16* xr = x + (int64_t)trow * a.D + 64 * wave + 32 * half;
-    const bf16* wr = W + (int64_t)col * a.D + 64 * wave + 32 * half;
-    double acc[16];
-    f32x16_t aacc, c;
+  const int ng = NG > wv ? (NG - wv + GM_KW - 1) / GM_KW : 0;   // groups of this wave
+  char* ring = reinterpret_cast<char*>(sm) + wv * (GM_RING * SLOT);
+  // instruction q fills rows 8q .. 8q+7 of the slot (q < 4: tokens, then gate columns);
+  // lane -> row 8q + lane/8, chunk lane%8 stored at position (lane%8) ^ (row%8)
+  const int lrow = lane >> 3, lch = lane & 7;
+  auto issue = [&](int m) {                       // the wave's m-th group
+    char* slot = ring + (m % GM_RING) * SLOT;
+    const int64_t k0 = (int64_t)64 * (wv + GM_KW * m);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) { acc[r] = 0.0; aacc[r] = 0.f; c[r] = 0.f; }
-    // every 2 chunks (32 products) the fp32 sums move to fp64; loads run one group ahead
-    uint4 xv[2][4], wv[2][4];
-    if (ng > 0) {
+    for (int q = 0; q < 4 * (1 + CB); ++q) {
+      const int r = 8 * q + lrow;
+      const int c = lch ^ (r & 7);
+      const bf16* src;
+      if (q < 4) src = x + (int64_t)min(t0 + r, a.T - 1) * a.D;
+      else src = W + (int64_t)min(r - 32, dM - 1) * a.D;
+      g2l16(src + k0 + 8 * c, slot + q * 1024);
+    }
+  };
+  // fragment of slot row `row`, chunk 4*half + jj
+  auto frag = [&](int m, int row, int jj) {
+    const char* slot = ring + (m % GM_RING) * SLOT;
+    const int c = (4 * half + jj) ^ (row & 7);
+    return *reinterpret_cast<const bf16x8_t*>(slot + row * 128 + c * 16);
+  };
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        xv[0][jj] = *reinterpret_cast<const uint4*>(xr + 8 * jj);
-        wv[0][jj] = *reinterpret_cast<const uint4*>(wr + 8 * jj);
+  for (int m = 0; m < GM_RING; ++m)
+    if (m < ng) issue(m);
+
+  double acc[CB][16];
+  f32x16_t aacc[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) { acc[cb][r] = 0.0; aacc[cb][r] = 0.f; }
+  for (int m = 0; m < ng; ++m) {
+    // Vector-memory operations retire in issue order, and group m is followed by the
+    // groups issued after it, LPG loads each: once at most that many are
+    // outstanding, group m has landed.
+    const int after = min(GM_RING - 1, ng - 1 - m);
+    const int n = LPG * after;
+    if (n >= 48) wait_vmcnt<48>(); else if (n >= 36) wait_vmcnt<36>(); else if (n >= 32) wait_vmcnt<32>();
+    else if (n >= 24) wait_vmcnt<24>(); else if (n >= 16) wait_vmcnt<16>(); else if (n >= 12) wait_vmcnt<12>();
+    else if (n >= 8) wait_vmcnt<8>(); else wait_vmcnt<0>();
+    f32x16_t c[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) c[cb][r] = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const bf16x8_t xq = frag(m, tok, jj);
+      const uint4 xu = __builtin_bit_cast(uint4, xq);
+      const uint4 xa = make_uint4(xu.x & 0x7fff7fffu, xu.y & 0x7fff7fffu, xu.z & 0x7fff7fffu, xu.w & 0x7fff7fffu);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        const bf16x8_t wq = frag(m, 32 + 32 * cb + tok, jj);
+        const uint4 wu = __builtin_bit_cast(uint4, wq);
+        const uint4 wa = make_uint4(wu.x & 0x7fff7fffu, wu.y & 0x7fff7fffu, wu.z & 0x7fff7fffu, wu.w & 0x7fff7fffu);
+        c[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wq, xq, c[cb], 0, 0, 0);
+        aacc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wa),
+                                                          __builtin_bit_cast(bf16x8_t, xa), aacc[cb], 0, 0, 0);
+      }
+      if (jj & 1) {                      // every 32 products the fp32 sums move to fp64
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) { acc[cb][r] += (double)c[cb][r]; c[cb][r] = 0.f; }
       }
     }
-    // one group: MFMAs on load slot SL while the next group loads into the other slot
-    auto group = [&](int gi, auto SLc) {
-      constexpr int SL = decltype(SLc)::value;
-      if (gi + 1 < ng) {
-        const int64_t o = (int64_t)256 * (gi + 1);
+    // every lane has read group m from its slot (the wave's LDS reads retire in order
+    // before the refill is issued); refill it with group m + RING
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0), vmcnt/expcnt untouched
+    asm volatile("" ::: "memory");
+    if (m + GM_RING < ng) issue(m + GM_RING);
+  }
+
+  // partial sums to LDS in wave order (rows padded to an odd word count: distinct
+  // banks per token), then one lane per token selects
+  wait_vmcnt<0>();
+  __syncthreads();                       // both rings drained before their memory is reused
+  const int SLD = dM + 1;
+  double* s64 = reinterpret_cast<double*>(sm);                 // [32][SLD]
+  float* ab = reinterpret_cast<float*>(s64 + GM_TOK * SLD);    // [32][SLD]
+  for (int w = 0; w < GM_KW; ++w) {
+    if (wv == w) {
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          xv[SL ^ 1][jj] = *reinterpret_cast<const uint4*>(xr + o + 8 * jj);
-          wv[SL ^ 1][jj] = *reinterpret_cast<const uint4*>(wr + o + 8 * jj);
-        }
-      }
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const uint4 xq = xv[SL][jj], wq = wv[SL][jj];
-        const uint4 xa = make_uint4(xq.x & 0x7fff7fffu, xq.y & 0x7fff7fffu, xq.z & 0x7fff7fffu, xq.w & 0x7fff7fffu);
-        const uint4 wa = make_uint4(wq.x & 0x7fff7fffu, wq.y & 0x7fff7fffu, wq.z & 0x7fff7fffu, wq.w & 0x7fff7fffu);
-        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wq), __builtin_bit_cast(bf16x8_t, xq),
-                                                   c, 0, 0, 0);
-        aacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, wa),
-                                                      __builtin_bit_cast(bf16x8_t, xa), aacc, 0, 0, 0);
-        if (jj & 1) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) { acc[r] += (double)c[r]; c[r] = 0.f; }
-        }
-      }
-    };
-    for (int gi = 0; gi < ng; gi += 2) {
-      group(gi, std::integral_constant<int, 0>{});
-      if (gi + 1 < ng) group(gi + 1, std::integral_constant<int, 1>{});
-    }
-    // lane holds token (lane % 32) and columns cb*32 + 8(r/4) + 4(lane/32) + r%4; the four
-    // waves' partial sums are added in wave order
-    for (int w = 0; w < 4; ++w) {
-      if (wave == w) {
+      for (int cb = 0; cb < CB; ++cb) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int cc = cb * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          const int cc = cb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
           if (cc < dM) {
             if (w == 0) {
-              s64[tok * SLD + cc] = acc[r] + (bg ? (double)bf2f(bg[cc]) : 0.0);
-              ab[tok * SLD + cc] = aacc[r];
+              s64[tok * SLD + cc] = acc[cb][r] + (bg ? (double)bf2f(bg[cc]) : 0.0);
+              ab[tok * SLD + cc] = aacc[cb][r];
             } else {
-              s64[tok * SLD + cc] += acc[r];
-              ab[tok * SLD + cc] += aacc[r];
+              s64[tok * SLD + cc] += acc[cb][r];
+              ab[tok * SLD + cc] += aacc[cb][r];
             }
           }
         }
       }
-      __syncthreads();
     }
+    __syncthreads();
   }
-  // selection: one thread per token; tokens without a certificate go to the queue
-  if (tid < GM_TOK && t0 + tid < a.T) {
-    const int t = t0 + tid;
-    const bool ok = select_token<true>(s64 + tid * SLD, ab + tid * SLD, a.alive, a.d, a.M, a.k, a.N, ga.gam,
+  if (threadIdx.x < GM_TOK && t0 + (int)threadIdx.x < a.T) {
+    const int t = t0 + threadIdx.x;
+    const bool ok = select_token<true>(s64 + lane * SLD, ab + lane * SLD, a.alive, a.d, a.M, a.k, a.N, ga.gam,
                                        a.idx + (int64_t)t * a.k, a.w + (int64_t)t * a.k,
                                        a.g ? a.g + (int64_t)t * a.k : nullptr);
     if (!ok) ga.queue[GQ_HEAD + atomicAdd(ga.queue, 1)] = t;
     if (ok && a.scores)
-      for (int c = 0; c < dM; ++c) a.scores[(int64_t)t * dM + c] = (float)s64[tid * SLD + c];
+      for (int c = 0; c < dM; ++c) a.scores[(int64_t)t * dM + c] = (float)s64[lane * SLD + c];
   }
 }
 
@@ -433,7 +509,9 @@ __global__ void __launch_bounds__(GX_NT) gate_exact_kernel(GateArgs a, const int
 }
 
 static size_t gate_mfma_lds_bytes(int dM) {
-  return (sizeof(double) + sizeof(float)) * GM_TOK * (dM + 1);
+  const size_t ring = (size_t)GM_KW * GM_RING * 4096 * (1 + (dM + 31) / 32);
+  const size_t scores = (sizeof(double) + sizeof(float)) * GM_TOK * (dM + 1);
+  return ring > scores ? ring : scores;
 }
 
 static size_t gate_lds_bytes(int dM) {
@@ -543,33 +621,34 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
   if (!aligned16(x) || !aligned16(Wg)) return DMOE_EUNSUPPORTED;
   GateArgs a{x, Wg, bg, alive, idx, w, g, scores, (int)s.T, (int)s.D, s.d, s.M, s.k, (int)s.dM, (int)s.N};
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (s.dtype == DMOE_BF16) {
+  if (s.dtype == DMOE_BF16 && s.dM <= 3 * 32) {
     if (!ws) return DMOE_EINVAL;
     if (!aligned16(ws)) return DMOE_EUNSUPPORTED;
-    // error factor of the MFMA scores (see select_token_cert)
+    // error factor of the MFMA scores (see the certificate above gate_topk_mfma)
     const double u = 1.0 / 8388608.0;
     const double g32 = 32 * u / (1 - 32 * u) + (s.D / 32 + 8) * 2.220446049250313e-16;
     const double gD = (double)s.D * u / (1 - (double)s.D * u);
     int32_t* queue = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + workspace_layout(s).gq_off);
     GateMfmaArgs ga{a, s.flags, (float)(g32 / (1 - gD) * 1.0001), queue};
     const size_t lds = gate_mfma_lds_bytes((int)s.dM);
-    static bool attr = false;
-    if (!attr) {
-      (void)hipFuncSetAttribute((const void*)gate_topk_mfma, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)gate_mfma_lds_bytes(DM_MAX));
+    const int CB = (int)((s.dM + 31) / 32);
+    auto kern = CB == 1 ? gate_topk_mfma<1> : CB == 2 ? gate_topk_mfma<2> : gate_topk_mfma<3>;
+    if (lds > 65536) {
+      (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       (void)hipGetLastError();
-      attr = true;
     }
     fill_zero(queue, sizeof(int32_t), st);
     const dim3 grid((unsigned)((s.T + GM_TOK - 1) / GM_TOK));
-    hipLaunchKernelGGL(gate_topk_mfma, grid, dim3(GM_NT), lds, st, ga);
+    hipLaunchKernelGGL(kern, grid, dim3(GM_NT), lds, st, ga);
     // exact recomputation of the queued tokens: persistent blocks over the queue
     const int xgrid = (int)std::min<int64_t>(s.T, 1024);
     hipLaunchKernelGGL(gate_exact_kernel, dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
   } else {
+    // fp32, and bf16 with more than 96 gate columns: exact fp64 scores for every token
     const dim3 grid((unsigned)((s.T + GATE_TB - 1) / GATE_TB));
     const size_t lds = gate_lds_bytes((int)s.dM);
-    hipLaunchKernelGGL(gate_topk_kernel<float>, grid, dim3(GATE_NT), lds, st, a);
+    if (s.dtype == DMOE_BF16) hipLaunchKernelGGL(gate_topk_kernel<bf16>, grid, dim3(GATE_NT), lds, st, a);
+    else hipLaunchKernelGGL(gate_topk_kernel<float>, grid, dim3(GATE_NT), lds, st, a);
   }
   return launch_status();
 }

@@ -31,6 +31,12 @@ CASES = {
     # 4-D grid, fp32
     "f32_grid4d": Workload("f32_grid4d", 15, T=200, D=64, H=64, d=4, M=3, k=5, dtype="f32",
                            act="gelu", p_alive=0.7),
+    # bf16 gate with 96 columns: three 32-column MFMA blocks per token group
+    "bf16_gate96": Workload("bf16_gate96", 16, T=300, D=192, H=128, d=2, M=48, k=3, dtype="bf16",
+                            act="gelu", p_alive=0.9),
+    # bf16 gate with 128 columns: the exact fp64 gate path
+    "bf16_gate128": Workload("bf16_gate128", 17, T=200, D=128, H=128, d=2, M=64, k=8, dtype="bf16",
+                             act="relu", p_alive=0.95),
 }
 
 
