@@ -24,9 +24,10 @@ PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 CALLS = ("gate_topk", "dispatch", "ffn_fwd", "combine", "combine_bwd", "gate_topk_bwd", "ffn_bwd",
          "dispatch_bwd")
+FWD_CALLS = ("gate_topk", "dispatch", "ffn_fwd", "combine")
 
 
-def algorithmic(wl, counts):
+def algorithmic(wl, counts, recompute=False):
     """Algorithmic bytes and flops per call (what the method must move/compute)."""
     e = 2 if wl.dtype == "bf16" else 4
     T, D, H, dM, k = wl.T, wl.D, wl.H, wl.dM, wl.k
@@ -44,6 +45,9 @@ def algorithmic(wl, counts):
     # dx_perm: read dh, W1; write dx_perm.  dW1: read dh, x_perm; write dW1.
     out["ffn_bwd"] = dict(bytes=2 * wbytes + rows * (D * e + 2 * H * e) + rows * (D * e + H * e)
                           + rows * (H * e + D * e) + rows * (H * e + D * e), flops=8 * rows * D * H)
+    if recompute:   # up-projection again: read x_perm and W1, write h and a
+        out["ffn_bwd"]["bytes"] += wbytes // 2 + rows * (D * e + 2 * H * e)
+        out["ffn_bwd"]["flops"] += 2 * rows * D * H
     out["dispatch_bwd"] = dict(bytes=rows * D * e + T * D * e + T * k * dM * 0, flops=0)
     return out
 
@@ -148,6 +152,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="wide")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--recompute", action="store_true",
+                    help="backward regenerates h and a (dmoe_expert_ffn_bwd_recompute)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -197,12 +203,17 @@ def main():
                                                          L.dw)),
             ("gate_topk_bwd", lambda: abi.dmoe_gate_topk_bwd(Dm, x, L.idx, L.w, L.dw, alive, L.dg, dWg, dbg,
                                                              L.ws)),
-            ("ffn_bwd", lambda: abi.dmoe_expert_ffn_bwd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
-                                                        L.dy_perm, W1, W2, L.dh, L.dx_perm, dW1, db1, dW2,
-                                                        db2, L.ws)),
+            ("ffn_bwd", (lambda: abi.dmoe_expert_ffn_bwd_recompute(Dm, L.offsets, L.counts, L.x_perm, W1, b1, W2,
+                                                                   L.dy_perm, L.h, L.a, L.dx_perm, dW1, db1,
+                                                                   dW2, db2, L.ws)) if args.recompute else
+             (lambda: abi.dmoe_expert_ffn_bwd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
+                                              L.dy_perm, W1, W2, L.dh, L.dx_perm, dW1, db1, dW2,
+                                              db2, L.ws))),
             ("dispatch_bwd", lambda: abi.dmoe_dispatch_bwd(Dm, L.dx_perm, L.pos, L.idx, L.dg, Wg, L.dx)),
         ]
         for name, fn in calls:
+            if not wl.backward and name not in FWD_CALLS:
+                continue
             if ev is not None:
                 ev[name][0].record(stream)
             fn()
@@ -214,7 +225,8 @@ def main():
     torch.cuda.synchronize()
     counts = L.counts.cpu().tolist()
 
-    evs = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in CALLS}
+    timed = [n for n in CALLS if wl.backward or n in FWD_CALLS]
+    evs = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in timed}
            for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -222,11 +234,11 @@ def main():
         step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in evs) / args.steps for n in CALLS}
+    ms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in evs) / args.steps for n in timed}
     print(f"[bench] {args.steps} steps in {wall:.3f} s; per call ms: " +
           ", ".join(f"{n} {v:.3f}" for n, v in ms.items()), file=sys.stderr, flush=True)
 
-    alg = algorithmic(wl, counts)
+    alg = algorithmic(wl, counts, args.recompute)
     peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
     ridge = peak_tf * 1e12 / (PEAK_HBM_GBS * 1e9)
 
@@ -261,9 +273,10 @@ def main():
         "data": "synthetic (seeded N(0,1) inputs, N(0,1/fan_in) weights, random init)",
         "config": {"workload": wl.name, "tokens": wl.T, "d_model": wl.D, "expert_hidden": wl.H,
                    "grid": f"{'x'.join([str(wl.M)] * wl.d)}", "experts": wl.N, "k": wl.k,
-                   "act": wl.act, "p_alive": wl.p_alive, "pass": "fwd+bwd"},
+                   "act": wl.act, "p_alive": wl.p_alive, "pass": "fwd+bwd" if wl.backward else "fwd",
+                   "activations": "recomputed in backward" if args.recompute else "stored"},
         "roofline": roofline,
-        "roofline_ffn_bwd": roof("ffn_bwd"),
+        "roofline_ffn_bwd": roof("ffn_bwd") if wl.backward else None,
         "gate_topk": roof("gate_topk"),
         "dispatch": roof("dispatch"),
         "calls_ms": {n: round(v, 4) for n, v in ms.items()},

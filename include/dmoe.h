@@ -167,6 +167,20 @@ int dmoe_expert_ffn_bwd(const dmoe_dims* dims, const int32_t* offsets, const int
                         const void* W1, const void* W2, void* dh, void* dx_perm, void* dW1,
                         void* db1, void* dW2, void* db2, void* ws, void* stream);
 
+/* The same backward with the forward's activations recomputed instead of kept
+ * (gradient checkpointing, as the Runtime's Backward does, Sec. 3.3 and App. E: it
+ * runs the expert's forward again when the gradient arrives; about one third more
+ * expert arithmetic, and h and a need not survive from the forward call):
+ *   h, a = x_perm W1_e^T + b1_e, act(.)   recomputed into the scratch h and a [P_max, H]
+ *   then exactly dmoe_expert_ffn_bwd with dh written over h.
+ * Outputs are bit-identical to dmoe_expert_ffn_bwd given the forward's h and a.
+ * h and a are caller-owned scratch (overwritten); b1 [N,H] is the up-projection bias.
+ * Uses workspace. */
+int dmoe_expert_ffn_bwd_recompute(const dmoe_dims* dims, const int32_t* offsets, const int32_t* counts,
+                                  const void* x_perm, const void* W1, const void* b1, const void* W2,
+                                  const void* dy_perm, void* h, void* a, void* dx_perm, void* dW1,
+                                  void* db1, void* dW2, void* db2, void* ws, void* stream);
+
 /* Input gradient of the layer: the experts' input gradients summed over each
  * token's alive pairs (slot order), plus, when idx, dg and Wg are all non-NULL,
  * the gate's share sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])].  fp32 accumulation,

@@ -21,7 +21,7 @@ DMOE_FLAG_GATE_EXACT = 1
 EXPORTS = (
     "dmoe_workspace_bytes", "dmoe_strerror", "dmoe_gate_topk", "dmoe_dispatch",
     "dmoe_expert_ffn_fwd", "dmoe_combine", "dmoe_combine_bwd", "dmoe_gate_topk_bwd",
-    "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd",
+    "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd", "dmoe_expert_ffn_bwd_recompute",
 )
 
 
@@ -65,6 +65,7 @@ def load(path=LIB_PATH):
         "dmoe_gate_topk_bwd": (ctypes.c_int, [pd] + [_P] * 10),
         "dmoe_expert_ffn_bwd": (ctypes.c_int, [pd] + [_P] * 16),
         "dmoe_dispatch_bwd": (ctypes.c_int, [pd] + [_P] * 7),
+        "dmoe_expert_ffn_bwd_recompute": (ctypes.c_int, [pd] + [_P] * 16),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -150,3 +151,11 @@ def dmoe_expert_ffn_bwd(dims, offsets, counts, x_perm, h, a, dy_perm, W1, W2, dh
 def dmoe_dispatch_bwd(dims, dx_perm, pos, idx, dg, Wg, dx, stream=None):
     _check(load().dmoe_dispatch_bwd(ctypes.byref(dims), _ptr(dx_perm), _ptr(pos), _ptr(idx), _ptr(dg),
                                     _ptr(Wg), _ptr(dx), _stream(stream)), "dmoe_dispatch_bwd")
+
+
+def dmoe_expert_ffn_bwd_recompute(dims, offsets, counts, x_perm, W1, b1, W2, dy_perm, h, a, dx_perm, dW1, db1,
+                                  dW2, db2, ws, stream=None):
+    _check(load().dmoe_expert_ffn_bwd_recompute(ctypes.byref(dims), _ptr(offsets), _ptr(counts), _ptr(x_perm),
+                                                _ptr(W1), _ptr(b1), _ptr(W2), _ptr(dy_perm), _ptr(h), _ptr(a),
+                                                _ptr(dx_perm), _ptr(dW1), _ptr(db1), _ptr(dW2), _ptr(db2),
+                                                _ptr(ws), _stream(stream)), "dmoe_expert_ffn_bwd_recompute")

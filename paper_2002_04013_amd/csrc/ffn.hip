@@ -171,6 +171,24 @@ static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
   }
 }
 
+// The up-projection of the forward alone (h = x W1^T + b1, a = act(h)), for the
+// recompute form of the backward.
+template <typename C>
+static void ffn_up_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, const bf16* W1, const bf16* b1,
+                        bf16* h, bf16* a, int32_t* tpre, hipStream_t st) {
+  const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
+  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  const int nt = (H + C::BN - 1) / C::BN;
+  GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
+  p.A = xp; p.lda = D;
+  p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
+  p.C = h; p.ldc = H; p.C2 = a;
+  p.bias = b1; p.bias_gstride = H;
+  p.N = H; p.K = D; p.act = s.act;
+  run_gemm2<GROUP_M, false, false, EPI_BIAS_ACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+}
+
 template <typename C, typename CW>
 static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, const bf16* h,
                          const bf16* a, const bf16* dyp, const bf16* W1, const bf16* W2, bf16* dh, bf16* dxp,
@@ -312,6 +330,22 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
 
 static bool use_fat(const Shape& s) { return s.P >= (int64_t)96 * s.N; }
 
+template <typename E, typename C>
+static void ffn_up_cfg(const Shape& s, const int32_t* offsets, const E* xp, const E* W1, const E* b1, E* h, E* a,
+                       int32_t* tpre, hipStream_t st) {
+  const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
+  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  const int nt = (H + C::BN - 1) / C::BN;
+  GemmArgs<E> p = args_m<E>(offsets, tpre, nt, N);
+  p.A = xp; p.lda = D;
+  p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
+  p.C = h; p.ldc = H; p.C2 = a;
+  p.bias = b1; p.bias_gstride = H;
+  p.N = H; p.K = D; p.act = s.act;
+  run_gemm<E, GROUP_M, true, EPI_BIAS_ACT, C::BM, C::BN, C::BK, C::WM, C::WN>(p, mt_ub * nt, st);
+}
+
 }  // namespace dmoe
 
 using namespace dmoe;
@@ -378,4 +412,37 @@ extern "C" int dmoe_expert_ffn_bwd(const dmoe_dims* dims, const int32_t* offsets
                                          m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
   }
   return launch_status();
+}
+
+extern "C" int dmoe_expert_ffn_bwd_recompute(const dmoe_dims* dims, const int32_t* offsets, const int32_t* counts,
+                                             const void* x_perm, const void* W1, const void* b1, const void* W2,
+                                             const void* dy_perm, void* h, void* a, void* dx_perm, void* dW1,
+                                             void* db1, void* dW2, void* db2, void* ws, void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s);
+  if (rc) return rc;
+  if (s.T == 0) return DMOE_OK;
+  if (!offsets || !x_perm || !W1 || !b1 || !W2 || !dy_perm || !h || !a || !dx_perm || !dW1 || !db1 || !dW2 ||
+      !db2 || !ws)
+    return DMOE_EINVAL;
+  for (const void* q : {x_perm, W1, W2, dy_perm, (const void*)h, (const void*)a, (const void*)dx_perm,
+                        (const void*)dW1, (const void*)db1, (const void*)dW2, (const void*)db2, (const void*)ws})
+    if (!aligned16(q)) return DMOE_EUNSUPPORTED;
+  const Workspace L = workspace_layout(s);
+  int32_t* tpre = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + L.tiles_off);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  // 1. recompute the up-projection of the forward into the scratch h and a
+  if (s.dtype == DMOE_BF16) {
+    auto c = [](const void* q) { return reinterpret_cast<const bf16*>(q); };
+    auto m = [](void* q) { return reinterpret_cast<bf16*>(q); };
+    if (use_fat(s)) ffn_up_bf16<G2Fat>(s, offsets, c(x_perm), c(W1), c(b1), m(h), m(a), tpre, st);
+    else ffn_up_bf16<G2Skinny>(s, offsets, c(x_perm), c(W1), c(b1), m(h), m(a), tpre, st);
+  } else {
+    auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };
+    auto m = [](void* q) { return reinterpret_cast<float*>(q); };
+    ffn_up_cfg<float, CfgF32>(s, offsets, c(x_perm), c(W1), c(b1), m(h), m(a), tpre, st);
+  }
+  // 2. the backward proper, dh written over h
+  return dmoe_expert_ffn_bwd(dims, offsets, counts, x_perm, h, a, dy_perm, W1, W2, h, dx_perm, dW1, db1, dW2,
+                             db2, ws, stream);
 }

@@ -3,6 +3,8 @@ the C-ABI calls for the forward and the backward pass.
 
 Forward:  gate_topk -> dispatch -> expert_ffn_fwd -> combine
 Backward: combine_bwd -> gate_topk_bwd -> expert_ffn_bwd -> dispatch_bwd
+With recompute=True the backward regenerates h and a (expert_ffn_bwd_recompute), so
+they need not be kept from the forward: h and a are then scratch shared by both passes.
 """
 import torch
 
@@ -13,9 +15,10 @@ class DMoELayer:
     """Device buffers for one layer shape; parameters are passed per call."""
 
     def __init__(self, T, D, H, d, M, k, dtype="bf16", act="gelu", device="cuda",
-                 dh_aliases_h=False, flags=0):
+                 dh_aliases_h=False, flags=0, recompute=False):
         self.dims = abi.make_dims(T, D, H, d, M, k, dtype, act, flags)
         self.T, self.D, self.H, self.d, self.M, self.k = T, D, H, d, M, k
+        self.recompute = recompute
         self.N = M ** d
         self.P = T * k
         self.dt = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -59,12 +62,20 @@ class DMoELayer:
         abi.dmoe_combine(D, self.y_perm, self.pos, self.w, self.y)
         return self.y
 
-    def backward(self, dy, x, Wg, alive, W1, W2, dW1, db1, dW2, db2, dWg, dbg):
+    def backward(self, dy, x, Wg, alive, W1, W2, dW1, db1, dW2, db2, dWg, dbg, b1=None):
+        """b1 is needed only with recompute=True (the up-projection is run again)."""
         D = self.dims
         abi.dmoe_combine_bwd(D, dy, self.y_perm, self.pos, self.w, self.dy_perm, self.dw)
         abi.dmoe_gate_topk_bwd(D, x, self.idx, self.w, self.dw, alive, self.dg, dWg, dbg, self.ws)
-        abi.dmoe_expert_ffn_bwd(D, self.offsets, self.counts, self.x_perm, self.h, self.a,
-                                self.dy_perm, W1, W2, self.dh, self.dx_perm, dW1, db1, dW2, db2,
-                                self.ws)
+        if self.recompute:
+            if b1 is None:
+                raise abi.DmoeError("recompute=True needs b1 in backward")
+            abi.dmoe_expert_ffn_bwd_recompute(D, self.offsets, self.counts, self.x_perm, W1, b1, W2,
+                                              self.dy_perm, self.h, self.a, self.dx_perm, dW1, db1, dW2,
+                                              db2, self.ws)
+        else:
+            abi.dmoe_expert_ffn_bwd(D, self.offsets, self.counts, self.x_perm, self.h, self.a,
+                                    self.dy_perm, W1, W2, self.dh, self.dx_perm, dW1, db1, dW2, db2,
+                                    self.ws)
         abi.dmoe_dispatch_bwd(D, self.dx_perm, self.pos, self.idx, self.dg, Wg, self.dx)
         return self.dx

@@ -34,15 +34,21 @@ def assert_close(gpu, ref, rtol, name):
                              f"gpu {g[i]!r} ref {r[i]!r} (rtol {rtol}, rms {rms:.3g})")
 
 
-def gpu_run(wl, inp, backward=True, dh_aliases_h=False, flags=0):
-    """Forward (and backward) through the C ABI on cuda:0; returns CPU copies."""
+def gpu_run(wl, inp, backward=True, dh_aliases_h=False, flags=0, recompute=False, clobber_h=False):
+    """Forward (and backward) through the C ABI on cuda:0; returns CPU copies.
+    recompute: backward through dmoe_expert_ffn_bwd_recompute; clobber_h: overwrite
+    h and a between the passes (they must not be needed then)."""
     from paper_2002_04013_amd import DMoELayer
     dev = torch.device("cuda")
     t = {n: v.to(dev) for n, v in inp.items()}
     L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, dh_aliases_h=dh_aliases_h,
-                  flags=flags)
+                  flags=flags, recompute=recompute)
     out = {}
     L.forward(t["x"], t["Wg"], t["bg"], t["alive"], t["W1"], t["b1"], t["W2"], t["b2"])
+    if clobber_h:
+        fwd_h, fwd_a = L.h.clone(), L.a.clone()
+        L.h.fill_(-3.0)
+        L.a.fill_(5.0)
     if backward:
         dt = L.dt
         sentinel = 7.0
@@ -52,12 +58,15 @@ def gpu_run(wl, inp, backward=True, dh_aliases_h=False, flags=0):
         db2 = torch.full_like(t["b2"], sentinel)
         dWg = torch.empty_like(t["Wg"])
         dbg = torch.empty_like(t["bg"])
-        L.backward(t["dy"], t["x"], t["Wg"], t["alive"], t["W1"], t["W2"], dW1, db1, dW2, db2, dWg, dbg)
+        L.backward(t["dy"], t["x"], t["Wg"], t["alive"], t["W1"], t["W2"], dW1, db1, dW2, db2, dWg, dbg,
+                   b1=t["b1"])
         out.update(dW1=dW1, db1=db1, dW2=dW2, db2=db2, dWg=dWg, dbg=dbg, dx=L.dx, dw=L.dw, dg=L.dg,
-                   dy_perm=L.dy_perm, dx_perm=L.dx_perm, dh=L.dh)
+                   dy_perm=L.dy_perm, dx_perm=L.dx_perm, dh=L.h if recompute else L.dh)
     torch.cuda.synchronize()
     out.update(idx=L.idx, w=L.w, g=L.g, scores=L.scores, counts=L.counts, offsets=L.offsets,
                row_token=L.row_token, pos=L.pos, x_perm=L.x_perm, h=L.h, a=L.a, y_perm=L.y_perm, y=L.y)
+    if clobber_h:
+        out.update(h=fwd_h, a=fwd_a)
     return {k: v.detach().cpu() for k, v in out.items()}
 
 
