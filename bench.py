@@ -27,7 +27,7 @@ CALLS = ("gate_topk", "dispatch", "ffn_fwd", "combine", "combine_bwd", "gate_top
 FWD_CALLS = ("gate_topk", "dispatch", "ffn_fwd", "combine")
 
 
-def algorithmic(wl, counts, recompute=False):
+def algorithmic(wl, counts, recompute=False, sgd=False):
     """Algorithmic bytes and flops per call (what the method must move/compute)."""
     e = 2 if wl.dtype == "bf16" else 4
     T, D, H, dM, k = wl.T, wl.D, wl.H, wl.dM, wl.k
@@ -45,6 +45,8 @@ def algorithmic(wl, counts, recompute=False):
     # dx_perm: read dh, W1; write dx_perm.  dW1: read dh, x_perm; write dW1.
     out["ffn_bwd"] = dict(bytes=2 * wbytes + rows * (D * e + 2 * H * e) + rows * (D * e + H * e)
                           + rows * (H * e + D * e) + rows * (H * e + D * e), flops=8 * rows * D * H)
+    if sgd:         # weight tiles read and written instead of dW written
+        out["ffn_bwd"]["bytes"] += wbytes // 2
     if recompute:   # up-projection again: read x_perm and W1, write h and a
         out["ffn_bwd"]["bytes"] += wbytes // 2 + rows * (D * e + 2 * H * e)
         out["ffn_bwd"]["flops"] += 2 * rows * D * H
@@ -154,6 +156,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--recompute", action="store_true",
                     help="backward regenerates h and a (dmoe_expert_ffn_bwd_recompute)")
+    ap.add_argument("--sgd", action="store_true",
+                    help="backward updates the expert parameters in place (dmoe_expert_ffn_bwd_sgd, lr 1e-4)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -203,9 +207,12 @@ def main():
                                                          L.dw)),
             ("gate_topk_bwd", lambda: abi.dmoe_gate_topk_bwd(Dm, x, L.idx, L.w, L.dw, alive, L.dg, dWg, dbg,
                                                              L.ws)),
-            ("ffn_bwd", (lambda: abi.dmoe_expert_ffn_bwd_recompute(Dm, L.offsets, L.counts, L.x_perm, W1, b1, W2,
-                                                                   L.dy_perm, L.h, L.a, L.dx_perm, dW1, db1,
-                                                                   dW2, db2, L.ws)) if args.recompute else
+            ("ffn_bwd", (lambda: abi.dmoe_expert_ffn_bwd_sgd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
+                                                             L.dy_perm, W1, b1, W2, b2, 1e-4, L.dh, L.dx_perm,
+                                                             L.ws)) if args.sgd else
+             (lambda: abi.dmoe_expert_ffn_bwd_recompute(Dm, L.offsets, L.counts, L.x_perm, W1, b1, W2,
+                                                        L.dy_perm, L.h, L.a, L.dx_perm, dW1, db1,
+                                                        dW2, db2, L.ws)) if args.recompute else
              (lambda: abi.dmoe_expert_ffn_bwd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
                                               L.dy_perm, W1, W2, L.dh, L.dx_perm, dW1, db1, dW2,
                                               db2, L.ws))),
@@ -238,7 +245,7 @@ def main():
     print(f"[bench] {args.steps} steps in {wall:.3f} s; per call ms: " +
           ", ".join(f"{n} {v:.3f}" for n, v in ms.items()), file=sys.stderr, flush=True)
 
-    alg = algorithmic(wl, counts, args.recompute)
+    alg = algorithmic(wl, counts, args.recompute, args.sgd)
     peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
     ridge = peak_tf * 1e12 / (PEAK_HBM_GBS * 1e9)
 
@@ -274,7 +281,8 @@ def main():
         "config": {"workload": wl.name, "tokens": wl.T, "d_model": wl.D, "expert_hidden": wl.H,
                    "grid": f"{'x'.join([str(wl.M)] * wl.d)}", "experts": wl.N, "k": wl.k,
                    "act": wl.act, "p_alive": wl.p_alive, "pass": "fwd+bwd" if wl.backward else "fwd",
-                   "activations": "recomputed in backward" if args.recompute else "stored"},
+                   "activations": "recomputed in backward" if args.recompute else "stored",
+                   "expert_update": "fused SGD in the backward" if args.sgd else "gradients returned"},
         "roofline": roofline,
         "roofline_ffn_bwd": roof("ffn_bwd") if wl.backward else None,
         "gate_topk": roof("gate_topk"),

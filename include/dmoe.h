@@ -181,6 +181,19 @@ int dmoe_expert_ffn_bwd_recompute(const dmoe_dims* dims, const int32_t* offsets,
                                   const void* dy_perm, void* h, void* a, void* dx_perm, void* dW1,
                                   void* db1, void* dW2, void* db2, void* ws, void* stream);
 
+/* The backward with the expert parameters updated by gradient descent in place
+ * (the Runtime's Backward updates its expert's parameters, Sec. 3.3):
+ *   W2_e <- W2_e - lr dy_perm_e^T a_e      b2_e <- b2_e - lr (sum of dy_perm_e rows)
+ *   W1_e <- W1_e - lr dh_e^T x_perm_e      b1_e <- b1_e - lr (sum of dh_e rows)
+ * with dh and dx_perm as in dmoe_expert_ffn_bwd, computed from the parameters as they
+ * were on entry.  The gradients are never stored: each update is applied from the
+ * fp32 accumulation and rounded once to the parameter dtype.  Experts with no rows
+ * keep their parameters.  dh may alias h.  lr must not be NaN.  Uses workspace. */
+int dmoe_expert_ffn_bwd_sgd(const dmoe_dims* dims, const int32_t* offsets, const int32_t* counts,
+                            const void* x_perm, const void* h, const void* a, const void* dy_perm,
+                            void* W1, void* b1, void* W2, void* b2, float lr, void* dh,
+                            void* dx_perm, void* ws, void* stream);
+
 /* Input gradient of the layer: the experts' input gradients summed over each
  * token's alive pairs (slot order), plus, when idx, dg and Wg are all non-NULL,
  * the gate's share sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])].  fp32 accumulation,

@@ -12,7 +12,8 @@ Neural Networks using Decentralized Mixture-of-Experts", arXiv 2002.04013):
     experts excluded and the rest renormalised (Sec. 3.1, Sec. 3.2);
   * grouping of (token, expert) pairs per expert (the Runtime batching of
     Sec. 3.3), the expert feed-forward blocks and the weighted sum of Eq. 1;
-  * the backward pass of all of the above.
+  * the backward pass of all of the above, and the gradient-descent update of an
+    expert's parameters that the Runtime's Backward applies (Sec. 3.3).
 
 Only tests/, __graft_entry__.smoke() and bench.py's CPU-baseline leg may import
 this package.  The product path never calls it, and it imports nothing from
@@ -23,7 +24,7 @@ from .dmoe import (
     to64, gate_scores, decision_scores, flat_index, uid_of, cell_totals,
     topk_bruteforce, topk_beam, topk_product_key, mixture_weights, act, act_grad,
     dispatch, expert_forward, expert_backward, gate_backward, layer_forward,
-    layer_backward, routing, chosen_totals, round_bf16, expert_forward_stored,
+    layer_backward, routing, chosen_totals, round_bf16, expert_forward_stored, round_f32, sgd_step,
 )
 
 __all__ = [
@@ -31,4 +32,5 @@ __all__ = [
     "topk_bruteforce", "topk_beam", "topk_product_key", "mixture_weights", "act",
     "act_grad", "dispatch", "expert_forward", "expert_backward", "gate_backward",
     "layer_forward", "layer_backward", "routing", "chosen_totals", "round_bf16", "expert_forward_stored",
+    "round_f32", "sgd_step",
 ]

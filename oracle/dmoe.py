@@ -241,6 +241,19 @@ def expert_backward(X, h, a, dY, W1, W2, kind, store=None):
 
 # ------------------------------------------------------------ dispatch (Sec. 3.3)
 
+def round_f32(a):
+    """fp32 rounding (round to nearest even) of fp64 values, returned in fp64."""
+    return np.asarray(a, np.float64).astype(np.float32).astype(np.float64)
+
+
+def sgd_step(param, grad, lr, store=None):
+    """Gradient-descent update of an expert's parameters, as the Runtime's Backward
+    applies it (Sec. 3.3): param - lr * grad, rounded once to the storage dtype by
+    `store` (round_bf16, round_f32, or None for exact)."""
+    store = store or _identity
+    return store(np.asarray(param, np.float64) - lr * np.asarray(grad, np.float64))
+
+
 def dispatch(idx, alive, N):
     """Group the alive (token, slot) pairs by expert, the way the Runtime collects
     the requests for each of its experts into one batch (Sec. 3.3).  Within an

@@ -3,10 +3,11 @@ a C ABI (include/dmoe.h, libdmoe.so) and a thin Python binding."""
 from . import abi
 from .abi import (DmoeError, Dims, make_dims, workspace_bytes, dmoe_gate_topk, dmoe_dispatch,
                   dmoe_expert_ffn_fwd, dmoe_combine, dmoe_combine_bwd, dmoe_gate_topk_bwd,
-                  dmoe_expert_ffn_bwd, dmoe_dispatch_bwd, dmoe_expert_ffn_bwd_recompute)
+                  dmoe_expert_ffn_bwd, dmoe_dispatch_bwd, dmoe_expert_ffn_bwd_recompute,
+                  dmoe_expert_ffn_bwd_sgd)
 from .layer import DMoELayer
 
 __all__ = ["abi", "DmoeError", "Dims", "make_dims", "workspace_bytes", "dmoe_gate_topk",
            "dmoe_dispatch", "dmoe_expert_ffn_fwd", "dmoe_combine", "dmoe_combine_bwd",
            "dmoe_gate_topk_bwd", "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd", "dmoe_expert_ffn_bwd_recompute",
-           "DMoELayer"]
+           "dmoe_expert_ffn_bwd_sgd", "DMoELayer"]

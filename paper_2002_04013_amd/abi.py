@@ -21,7 +21,7 @@ DMOE_FLAG_GATE_EXACT = 1
 EXPORTS = (
     "dmoe_workspace_bytes", "dmoe_strerror", "dmoe_gate_topk", "dmoe_dispatch",
     "dmoe_expert_ffn_fwd", "dmoe_combine", "dmoe_combine_bwd", "dmoe_gate_topk_bwd",
-    "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd", "dmoe_expert_ffn_bwd_recompute",
+    "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd", "dmoe_expert_ffn_bwd_recompute", "dmoe_expert_ffn_bwd_sgd",
 )
 
 
@@ -66,6 +66,7 @@ def load(path=LIB_PATH):
         "dmoe_expert_ffn_bwd": (ctypes.c_int, [pd] + [_P] * 16),
         "dmoe_dispatch_bwd": (ctypes.c_int, [pd] + [_P] * 7),
         "dmoe_expert_ffn_bwd_recompute": (ctypes.c_int, [pd] + [_P] * 16),
+        "dmoe_expert_ffn_bwd_sgd": (ctypes.c_int, [pd] + [_P] * 10 + [ctypes.c_float] + [_P] * 4),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -159,3 +160,11 @@ def dmoe_expert_ffn_bwd_recompute(dims, offsets, counts, x_perm, W1, b1, W2, dy_
                                                 _ptr(W1), _ptr(b1), _ptr(W2), _ptr(dy_perm), _ptr(h), _ptr(a),
                                                 _ptr(dx_perm), _ptr(dW1), _ptr(db1), _ptr(dW2), _ptr(db2),
                                                 _ptr(ws), _stream(stream)), "dmoe_expert_ffn_bwd_recompute")
+
+
+def dmoe_expert_ffn_bwd_sgd(dims, offsets, counts, x_perm, h, a, dy_perm, W1, b1, W2, b2, lr, dh, dx_perm, ws,
+                            stream=None):
+    _check(load().dmoe_expert_ffn_bwd_sgd(ctypes.byref(dims), _ptr(offsets), _ptr(counts), _ptr(x_perm), _ptr(h),
+                                          _ptr(a), _ptr(dy_perm), _ptr(W1), _ptr(b1), _ptr(W2), _ptr(b2),
+                                          ctypes.c_float(lr), _ptr(dh), _ptr(dx_perm), _ptr(ws), _stream(stream)),
+           "dmoe_expert_ffn_bwd_sgd")

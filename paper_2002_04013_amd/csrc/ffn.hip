@@ -51,9 +51,11 @@ tile_plan(const int32_t* offsets, int N, int BM, int32_t* plan) {
 
 // out[e][c] = sum of rows [offsets[e], offsets[e+1]) of X[:, c]  (bias gradients);
 // experts without rows are skipped (their slots are left untouched).
-template <typename E>
+// out[e][c] = sum of rows [offsets[e], offsets[e+1]) of column c (experts without rows
+// are left untouched); SGD: out[e][c] -= lr * that sum (out holds the parameters).
+template <typename E, bool SGD = false>
 __global__ void __launch_bounds__(256)
-segment_colsum(const E* X, int64_t ld, const int32_t* offsets, int ncols, E* out) {
+segment_colsum(const E* X, int64_t ld, const int32_t* offsets, int ncols, E* out, float lr = 0.f) {
   constexpr int VEC = 16 / sizeof(E);
   const int e = blockIdx.y;
   const int r0 = offsets[e], r1 = offsets[e + 1];
@@ -69,7 +71,14 @@ segment_colsum(const E* X, int64_t ld, const int32_t* offsets, int ncols, E* out
 #pragma unroll
     for (int i = 0; i < VEC; ++i) acc[i] += v[i];
   }
-  *reinterpret_cast<uint4*>(out + (int64_t)e * ncols + c) = Vec<E>::pack(acc);
+  uint4* op = reinterpret_cast<uint4*>(out + (int64_t)e * ncols + c);
+  if constexpr (SGD) {
+    float w[VEC];
+    Vec<E>::unpack(*op, w);
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) acc[i] = w[i] - lr * acc[i];
+  }
+  *op = Vec<E>::pack(acc);
 }
 
 static int device_cus() {
@@ -240,6 +249,60 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
                      st, dyp, (int64_t)D, offsets, D, db2);
 }
 
+// Backward with the expert parameters updated in place (W <- W - lr dW, b <- b - lr db),
+// the gradients never stored.  Each parameter is updated after its last use: dh reads
+// W2 before W2's update, dx_perm reads W1 before W1's update.
+template <typename C, typename CW>
+static void ffn_bwd_sgd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, const bf16* a,
+                             const bf16* dyp, bf16* W1, bf16* b1, bf16* W2, bf16* b2, float lr, const bf16* h,
+                             bf16* dh, bf16* dxp, int32_t* tpre, hipStream_t st) {
+  const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
+  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  const int64_t active_ub = std::min<int64_t>(s.N, s.P);
+  const int32_t* tact = tpre + N + 1;
+  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  {   // dh = (dy W2) * act'(h)
+    const int nt = (H + C::BN - 1) / C::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
+    p.A = dyp; p.lda = D;
+    p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
+    p.C = dh; p.ldc = H; p.aux = h;
+    p.N = H; p.K = D; p.act = s.act;
+    run_gemm2<GROUP_M, false, true, EPI_DACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+  }
+  {   // W2_e -= lr dy_e^T a_e
+    const int mt = (D + CW::BM - 1) / CW::BM, nt = (H + CW::BN - 1) / CW::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tact, mt * nt, N);
+    p.A = dyp; p.lda = D;
+    p.B = a; p.ldb = H;
+    p.C = W2; p.ldc = H; p.c_gstride = (int64_t)D * H;
+    p.M = D; p.N = H; p.act = s.act; p.lr = lr;
+    run_gemm2<GROUP_K, true, true, EPI_SGD, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
+  }
+  {   // dx_perm = dh W1
+    const int nt = (D + C::BN - 1) / C::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
+    p.A = dh; p.lda = H;
+    p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
+    p.C = dxp; p.ldc = D;
+    p.N = D; p.K = H; p.act = s.act;
+    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+  }
+  {   // W1_e -= lr dh_e^T x_e
+    const int mt = (H + CW::BM - 1) / CW::BM, nt = (D + CW::BN - 1) / CW::BN;
+    GemmArgs<bf16> p = args_m<bf16>(offsets, tact, mt * nt, N);
+    p.A = dh; p.lda = H;
+    p.B = xp; p.ldb = D;
+    p.C = W1; p.ldc = D; p.c_gstride = (int64_t)H * D;
+    p.M = H; p.N = D; p.act = s.act; p.lr = lr;
+    run_gemm2<GROUP_K, true, true, EPI_SGD, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
+  }
+  hipLaunchKernelGGL((segment_colsum<bf16, true>), dim3((unsigned)((H / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
+                     st, dh, (int64_t)H, offsets, H, b1, lr);
+  hipLaunchKernelGGL((segment_colsum<bf16, true>), dim3((unsigned)((D / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
+                     st, dyp, (int64_t)D, offsets, D, b2, lr);
+}
+
 template <typename E, typename C>
 static void ffn_fwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, const E* W1,
                         const E* b1, const E* W2, const E* b2, E* h, E* a, E* yp, int32_t* tpre,
@@ -271,10 +334,14 @@ static void ffn_fwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   }
 }
 
-template <typename E, typename C, typename CW>
+// SGD: dW1, db1, dW2, db2 are the parameters W1, b1, W2, b2 themselves, updated in
+// place (W <- W - lr dW) after their last read: dh reads W2 before W2's update and
+// dx_perm reads W1 before W1's update.
+template <typename E, typename C, typename CW, bool SGD = false>
 static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, const E* h,
                         const E* a, const E* dyp, const E* W1, const E* W2, E* dh, E* dxp, E* dW1,
-                        E* db1, E* dW2, E* db2, int32_t* tpre, hipStream_t st) {
+                        E* db1, E* dW2, E* db2, int32_t* tpre, hipStream_t st, float lr = 0.f) {
+  constexpr int EPI_W = SGD ? EPI_SGD : EPI_STORE;
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
   const int64_t active_ub = std::min<int64_t>(s.N, s.P);
@@ -297,8 +364,8 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
     p.A = dyp; p.lda = D;
     p.B = a; p.ldb = H;
     p.C = dW2; p.ldc = H; p.c_gstride = (int64_t)D * H;
-    p.M = D; p.N = H; p.act = s.act;
-    run_gemm<E, GROUP_K, false, EPI_STORE, CW::BM, CW::BN, CW::BK, CW::WM, CW::WN>(p, active_ub * mt * nt, st);
+    p.M = D; p.N = H; p.act = s.act; p.lr = lr;
+    run_gemm<E, GROUP_K, false, EPI_W, CW::BM, CW::BN, CW::BK, CW::WM, CW::WN>(p, active_ub * mt * nt, st);
   }
   // dx_perm = dh W1              B = W1_e viewed as (n = d, k = h): N-contiguous
   {
@@ -317,15 +384,15 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
     p.A = dh; p.lda = H;
     p.B = xp; p.ldb = D;
     p.C = dW1; p.ldc = D; p.c_gstride = (int64_t)H * D;
-    p.M = H; p.N = D; p.act = s.act;
-    run_gemm<E, GROUP_K, false, EPI_STORE, CW::BM, CW::BN, CW::BK, CW::WM, CW::WN>(p, active_ub * mt * nt, st);
+    p.M = H; p.N = D; p.act = s.act; p.lr = lr;
+    run_gemm<E, GROUP_K, false, EPI_W, CW::BM, CW::BN, CW::BK, CW::WM, CW::WN>(p, active_ub * mt * nt, st);
   }
   // bias gradients
   constexpr int VEC = 16 / sizeof(E);
-  hipLaunchKernelGGL(segment_colsum<E>, dim3((unsigned)((H / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
-                     st, dh, (int64_t)H, offsets, H, db1);
-  hipLaunchKernelGGL(segment_colsum<E>, dim3((unsigned)((D / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
-                     st, dyp, (int64_t)D, offsets, D, db2);
+  hipLaunchKernelGGL((segment_colsum<E, SGD>), dim3((unsigned)((H / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
+                     st, dh, (int64_t)H, offsets, H, db1, lr);
+  hipLaunchKernelGGL((segment_colsum<E, SGD>), dim3((unsigned)((D / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
+                     st, dyp, (int64_t)D, offsets, D, db2, lr);
 }
 
 static bool use_fat(const Shape& s) { return s.P >= (int64_t)96 * s.N; }
@@ -445,4 +512,40 @@ extern "C" int dmoe_expert_ffn_bwd_recompute(const dmoe_dims* dims, const int32_
   // 2. the backward proper, dh written over h
   return dmoe_expert_ffn_bwd(dims, offsets, counts, x_perm, h, a, dy_perm, W1, W2, h, dx_perm, dW1, db1, dW2,
                              db2, ws, stream);
+}
+
+extern "C" int dmoe_expert_ffn_bwd_sgd(const dmoe_dims* dims, const int32_t* offsets, const int32_t* counts,
+                                       const void* x_perm, const void* h, const void* a, const void* dy_perm,
+                                       void* W1, void* b1, void* W2, void* b2, float lr, void* dh, void* dx_perm,
+                                       void* ws, void* stream) {
+  (void)counts;
+  Shape s;
+  int rc = check_dims(dims, &s);
+  if (rc) return rc;
+  if (s.T == 0) return DMOE_OK;
+  if (!offsets || !x_perm || !h || !a || !dy_perm || !W1 || !b1 || !W2 || !b2 || !dh || !dx_perm || !ws)
+    return DMOE_EINVAL;
+  if (!(lr == lr)) return DMOE_EINVAL;                       // NaN step size
+  for (const void* q : {x_perm, h, a, dy_perm, (const void*)W1, (const void*)b1, (const void*)W2,
+                        (const void*)b2, (const void*)dh, (const void*)dx_perm, (const void*)ws})
+    if (!aligned16(q)) return DMOE_EUNSUPPORTED;
+  const Workspace L = workspace_layout(s);
+  int32_t* tpre = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + L.tiles_off);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (s.dtype == DMOE_BF16) {
+    auto c = [](const void* q) { return reinterpret_cast<const bf16*>(q); };
+    auto m = [](void* q) { return reinterpret_cast<bf16*>(q); };
+    if (use_fat(s))
+      ffn_bwd_sgd_bf16<G2Fat, G2DW>(s, offsets, c(x_perm), c(a), c(dy_perm), m(W1), m(b1), m(W2), m(b2), lr,
+                                    c(h), m(dh), m(dx_perm), tpre, st);
+    else
+      ffn_bwd_sgd_bf16<G2Skinny, G2DW>(s, offsets, c(x_perm), c(a), c(dy_perm), m(W1), m(b1), m(W2), m(b2), lr,
+                                       c(h), m(dh), m(dx_perm), tpre, st);
+  } else {
+    auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };
+    auto m = [](void* q) { return reinterpret_cast<float*>(q); };
+    ffn_bwd_cfg<float, CfgF32, CfgDWF32, true>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
+                                               m(dx_perm), m(W1), m(b1), m(W2), m(b2), tpre, st, lr);
+  }
+  return launch_status();
 }

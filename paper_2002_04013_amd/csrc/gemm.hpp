@@ -17,7 +17,8 @@
 namespace dmoe {
 
 enum GroupMode { GROUP_M = 0, GROUP_K = 1 };
-enum Epilogue { EPI_STORE = 0, EPI_BIAS = 1, EPI_BIAS_ACT = 2, EPI_DACT = 3, EPI_F32 = 4 };
+// EPI_SGD: C holds parameters; C <- C - lr * (A^T B) (the gradient is not stored)
+enum Epilogue { EPI_STORE = 0, EPI_BIAS = 1, EPI_BIAS_ACT = 2, EPI_DACT = 3, EPI_F32 = 4, EPI_SGD = 5 };
 
 template <typename E> struct Mma;
 template <> struct Mma<bf16> {
@@ -52,6 +53,7 @@ struct GemmArgs {
   int M, N, K;                                     // fixed dims (M unused for GROUP_M, K for GROUP_K)
   int act;
   int chunked;                                     // XCD-chunked schedule (grid >= 8)
+  float lr;                                        // EPI_SGD: step size
 };
 
 // K-contiguous tile (R rows x BK): element (r, k) at base[r * ld + k].
@@ -306,6 +308,11 @@ grouped_gemm(GemmArgs<E> p) {
             const E* hp = p.aux + crow + n;
 #pragma unroll
             for (int r = 0; r < 4; ++r) v[r] *= act_bwd(ldf(hp + r), p.act);
+          }
+          if constexpr (EPI == EPI_SGD) {
+            const E* wp = reinterpret_cast<const E*>(p.C) + crow + n;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = ldf(wp + r) - p.lr * v[r];
           }
           if constexpr (EPI == EPI_F32) {
             *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) =

@@ -385,7 +385,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
     // and the remaining stages are issued after the epilogue.
     const int l32 = lane & 31, lhi = lane >> 5;
     constexpr bool HAS_BIAS = EPI == EPI_BIAS || EPI == EPI_BIAS_ACT;
-    constexpr bool HAS_AUX = EPI == EPI_DACT;
+    constexpr bool HAS_AUX = EPI == EPI_DACT || EPI == EPI_SGD;   // reads a tile in C's layout
     constexpr int PRE = HAS_AUX ? 1 : STAGES;       // prologue stages issued before the epilogue
     uint2 bias_v[HAS_BIAS ? TN : 1][4];
     if constexpr (HAS_BIAS) {
@@ -419,17 +419,22 @@ grouped_gemm2(GemmArgs<bf16> p) {
       if constexpr (GM == GROUP_M) crow = (int64_t)(off + m0 + ml) * p.ldc;
       else crow = (int64_t)e * p.c_gstride + (int64_t)(m0 + ml) * p.ldc;
       const bool mok = ml < mvalid;
-      // h of this 32-row block for the activation derivative, all loaded before the
-      // block's first store (a load issued after a store also waits for the store)
+      // this 32-row block of the tile read in C's layout (h for the activation
+      // derivative; the parameters themselves for the SGD update), all loaded before
+      // the block's first store (a load issued after a store also waits for the store)
       uint2 aux_v[HAS_AUX ? TN : 1][4];
       if constexpr (HAS_AUX) {
-        const int64_t arow = (int64_t)(off + m0 + (mok ? ml : 0)) * p.ldc;
+        const int mr = mok ? ml : 0;
+        int64_t arow;
+        if constexpr (GM == GROUP_M) arow = (int64_t)(off + m0 + mr) * p.ldc;
+        else arow = (int64_t)e * p.c_gstride + (int64_t)(m0 + mr) * p.ldc;
+        const bf16* src = EPI == EPI_SGD ? reinterpret_cast<const bf16*>(p.C) : p.aux;
 #pragma unroll
         for (int i = 0; i < TN; ++i)
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int nl_ = wn * WTN + i * 32 + 8 * g + 4 * lhi;
-            aux_v[i][g] = *reinterpret_cast<const uint2*>(p.aux + arow + n0 + (nl_ < nvalid ? nl_ : 0));
+            aux_v[i][g] = *reinterpret_cast<const uint2*>(src + arow + n0 + (nl_ < nvalid ? nl_ : 0));
           }
       }
 #pragma unroll
@@ -447,12 +452,19 @@ grouped_gemm2(GemmArgs<bf16> p) {
             v[0] += __uint_as_float(b.x << 16); v[1] += __uint_as_float(b.x & 0xffff0000u);
             v[2] += __uint_as_float(b.y << 16); v[3] += __uint_as_float(b.y & 0xffff0000u);
           }
-          if constexpr (HAS_AUX) {
+          if constexpr (EPI == EPI_DACT) {
             const uint2 hv = aux_v[i][g];
             v[0] *= act_bwd_fast(__uint_as_float(hv.x << 16), p.act);
             v[1] *= act_bwd_fast(__uint_as_float(hv.x & 0xffff0000u), p.act);
             v[2] *= act_bwd_fast(__uint_as_float(hv.y << 16), p.act);
             v[3] *= act_bwd_fast(__uint_as_float(hv.y & 0xffff0000u), p.act);
+          }
+          if constexpr (EPI == EPI_SGD) {
+            const uint2 wv = aux_v[i][g];
+            v[0] = __uint_as_float(wv.x << 16) - p.lr * v[0];
+            v[1] = __uint_as_float(wv.x & 0xffff0000u) - p.lr * v[1];
+            v[2] = __uint_as_float(wv.y << 16) - p.lr * v[2];
+            v[3] = __uint_as_float(wv.y & 0xffff0000u) - p.lr * v[3];
           }
           if constexpr (EPI == EPI_F32) {
             *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) = make_float4(v[0], v[1], v[2], v[3]);

@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 import torch
 
-from parity_util import assert_close, compare, gpu_run, oracle_run, say
+from parity_util import RTOL, assert_close, compare, gpu_run, oracle_run, say
 from workloads import Workload, make_inputs, small_workload
 
 pytestmark = pytest.mark.gpu
@@ -200,3 +200,62 @@ def test_recompute_backward(name):
         assert torch.equal(a[n][:rows], b[n][:rows]), n
     fwd, bwd = oracle_run(wl, inp)
     compare(wl, inp, b, fwd, bwd)
+
+
+def _ulp(ref, dtype):
+    """One unit in the last place of |ref| in the storage dtype (bf16: 8 significant
+    bits, fp32: 24), for ref != 0; the smallest normal's for ref == 0."""
+    bits = 8 if dtype == "bf16" else 24
+    e = np.floor(np.log2(np.maximum(np.abs(ref), 2.0 ** -126)))
+    return 2.0 ** (e - bits + 1)
+
+
+@pytest.mark.parametrize("name", ["bf16_skinny", "bf16_fat", "f32_grid4d"])
+def test_sgd_backward(name):
+    """dmoe_expert_ffn_bwd_sgd: dh and dx_perm bit-identical to the plain backward
+    (computed from the parameters on entry); each parameter becomes
+    store(W - lr dW) of the oracle's dW within one unit of the storage dtype's last
+    place plus the dW tolerance; experts without rows keep their parameters bit for
+    bit.  lr is scaled so the update is about a quarter of the weights' magnitude."""
+    import oracle as O
+    from paper_2002_04013_amd import DMoELayer, abi
+    wl = CASES[name]
+    say(f"[parity] sgd backward {name}")
+    inp = make_inputs(wl, "cpu")
+    ref = gpu_run(wl, inp)
+    fwd, bwd = oracle_run(wl, inp)
+    rms = lambda v: float(np.sqrt(np.mean(np.square(v)))) if v.size else 1.0
+    # dense oracle gradients (zero for experts without rows)
+    grads = {}
+    for q, n in enumerate(("dW1", "db1", "dW2", "db2")):
+        g = np.zeros(inp[n[1:]].shape)
+        for e, gr in bwd["expert_grads"].items():
+            g[e] = gr[q]
+        grads[n] = g
+    lr = 0.25 * rms(O.to64(inp["W1"])) / max(rms(grads["dW1"][ref["counts"].numpy() > 0]), 1e-30)
+    dev = torch.device("cuda")
+    t = {n: v.to(dev) for n, v in inp.items()}
+    L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act)
+    L.forward(t["x"], t["Wg"], t["bg"], t["alive"], t["W1"], t["b1"], t["W2"], t["b2"])
+    abi.dmoe_combine_bwd(L.dims, t["dy"], L.y_perm, L.pos, L.w, L.dy_perm, L.dw)
+    P = {n: t[n].clone() for n in ("W1", "b1", "W2", "b2")}
+    abi.dmoe_expert_ffn_bwd_sgd(L.dims, L.offsets, L.counts, L.x_perm, L.h, L.a, L.dy_perm, P["W1"], P["b1"],
+                                P["W2"], P["b2"], lr, L.dh, L.dx_perm, L.ws)
+    torch.cuda.synchronize()
+    rows = int(ref["offsets"][-1])
+    assert torch.equal(L.dh[:rows].cpu(), ref["dh"][:rows]), "dh"
+    assert torch.equal(L.dx_perm[:rows].cpu(), ref["dx_perm"][:rows]), "dx_perm"
+    store = O.round_bf16 if wl.dtype == "bf16" else O.round_f32
+    counts = ref["counts"].numpy()
+    rtol = RTOL[wl.dtype]
+    for n, g in (("W1", "dW1"), ("b1", "db1"), ("W2", "dW2"), ("b2", "db2")):
+        old = O.to64(inp[n])
+        want = O.sgd_step(old, grads[g], lr, store)
+        got = O.to64(P[n].cpu())
+        live = counts > 0
+        dg = grads[g][live]
+        tol = _ulp(want[live], wl.dtype) + lr * rtol * (np.abs(dg) + rms(dg))
+        assert np.all(np.abs(got[live] - want[live]) <= tol), n
+        np.testing.assert_array_equal(got[~live], old[~live], n + " (experts without rows)")
+        if n in ("W1", "W2"):   # the update is visible, not absorbed by the rounding
+            assert np.median(np.abs(got[live] - old[live])) > 2 * np.median(_ulp(old[live], wl.dtype)), n

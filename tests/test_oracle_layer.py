@@ -335,3 +335,19 @@ def test_storage_rounding_only_perturbs_at_bf16_level():
     for n in ("dx", "dWg"):
         rms = np.sqrt(np.mean(b0[n] ** 2))
         assert np.max(np.abs(b1[n] - b0[n])) < 2 ** -5 * rms, n
+
+
+def test_sgd_step_pins():
+    """W - lr dW with one rounding to the storage dtype."""
+    W = np.array([1.0, -2.0, 0.5, 3.0])
+    g = np.array([2.0, -4.0, 0.25, 0.0])
+    np.testing.assert_array_equal(O.sgd_step(W, g, 0.5), [0.0, 0.0, 0.375, 3.0])
+    np.testing.assert_array_equal(O.sgd_step(W, g, 0.0), W)
+    # just below 1 the bf16 values (8 significant bits) are 2^-8 apart: 1 - 2^-8 and 1.
+    # 1 - 2^-9 is the halfway case and rounds to the even significand, 1.0;
+    # 1 - 3 * 2^-10 is nearer to 1 - 2^-8
+    assert O.sgd_step(np.array([1.0]), np.array([2.0 ** -9]), 1.0, O.round_bf16)[0] == 1.0
+    assert O.sgd_step(np.array([1.0]), np.array([3 * 2.0 ** -10]), 1.0, O.round_bf16)[0] == 1.0 - 2.0 ** -8
+    # fp32 rounding: 1 + 2^-25 is below half an ulp of 1 (2^-24)
+    assert O.sgd_step(np.array([1.0]), np.array([-(2.0 ** -25)]), 1.0, O.round_f32)[0] == 1.0
+    assert O.sgd_step(np.array([1.0]), np.array([-(2.0 ** -23)]), 1.0, O.round_f32)[0] == 1.0 + 2.0 ** -23
