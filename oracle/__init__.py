@@ -7,7 +7,8 @@ Neural Networks using Decentralized Mixture-of-Experts", arXiv 2002.04013):
   * the grid-factored gate, d linear layers g_i whose scores add up over the
     expert grid (Sec. 3.2, restated in App. C);
   * TopK over the grid, by brute force over every cell, by the beam search of
-    App. C (Algorithm 1) and by the product-key shortcut App. C points to;
+    App. C (Algorithm 1) and by the product-key shortcut App. C points to, and
+    TopK among the alive experts only (brute force);
   * the Eq. 1 softmax weights over the chosen experts, with non-responding
     experts excluded and the rest renormalised (Sec. 3.1, Sec. 3.2);
   * grouping of (token, expert) pairs per expert (the Runtime batching of
@@ -22,7 +23,7 @@ brute force, library routines, closed forms, autograd or hand-worked cases.
 """
 from .dmoe import (
     to64, gate_scores, decision_scores, flat_index, uid_of, cell_totals,
-    topk_bruteforce, topk_beam, topk_product_key, mixture_weights, act, act_grad,
+    topk_bruteforce, topk_beam, topk_product_key, topk_alive_bruteforce, mixture_weights, act, act_grad,
     dispatch, expert_forward, expert_backward, gate_backward, layer_forward,
     layer_backward, routing, chosen_totals, round_bf16, expert_forward_stored, round_f32, sgd_step,
 )
@@ -32,5 +33,5 @@ __all__ = [
     "topk_bruteforce", "topk_beam", "topk_product_key", "mixture_weights", "act",
     "act_grad", "dispatch", "expert_forward", "expert_backward", "gate_backward",
     "layer_forward", "layer_backward", "routing", "chosen_totals", "round_bf16", "expert_forward_stored",
-    "round_f32", "sgd_step",
+    "round_f32", "sgd_step", "topk_alive_bruteforce",
 ]

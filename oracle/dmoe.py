@@ -141,6 +141,27 @@ def topk_beam(S32, d, M, k, active_suffixes=None):
     return np.array(out_idx, np.int64), np.array(out_g, np.float64)
 
 
+def topk_alive_bruteforce(S32, d, M, k, alive):
+    """TopK among the experts that respond (the partially populated grid of App. C,
+    whose Algorithm 1 only extends prefixes with active suffixes): every cell of the
+    grid ranked by (alive first, total desc, flat asc) and the k first kept, so the
+    k best alive experts are chosen; when fewer than k are alive, the best dead
+    cells fill the remaining places (they get weight 0 in Eq. 1)."""
+    g = cell_totals(S32, d, M)                       # [T, N]
+    T, N = g.shape
+    if k > N:
+        raise ValueError("k > number of experts")
+    live = np.asarray(alive, bool).reshape(-1)
+    ids = np.arange(N)
+    idx = np.empty((T, k), np.int64)
+    gg = np.empty((T, k), np.float64)
+    for t in range(T):
+        order = np.lexsort((ids, -g[t], ~live))[:k]     # last key sorts first: alive, total, flat
+        idx[t] = order
+        gg[t] = g[t, order]
+    return idx, gg
+
+
 def topk_product_key(S32, d, M, k):
     """Centralised top-k search App. C refers to (product-key layers): the k best
     cells of an additive score lie in the Cartesian product of the per-dimension
@@ -287,12 +308,16 @@ def chosen_totals(S, idx, d, M):
     return g
 
 
-def routing(x, Wg, bg, alive, d, M, k):
+def routing(x, Wg, bg, alive, d, M, k, alive_topk=False):
     """Gate, TopK and Eq. 1 weights for a batch of tokens.  TopK compares the fp32
-    decision scores; the weights use the exact totals of the chosen experts."""
+    decision scores; the weights use the exact totals of the chosen experts.
+    alive_topk: TopK among the alive experts (topk_alive_bruteforce)."""
     S = gate_scores(x, Wg, bg)
     S32 = decision_scores(S)
-    idx, g32 = topk_bruteforce(S32, d, M, k)
+    if alive_topk:
+        idx, g32 = topk_alive_bruteforce(S32, d, M, k, np.ones(M ** d) if alive is None else alive)
+    else:
+        idx, g32 = topk_bruteforce(S32, d, M, k)
     g = chosen_totals(S, idx, d, M)
     w = mixture_weights(g, idx, alive)
     return dict(S=S, S32=S32, idx=idx, g32=g32, g=g, w=w)
@@ -305,7 +330,7 @@ def _expert_getter(experts):
     return lambda e: (W1[e], b1[e], W2[e], b2[e])
 
 
-def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, store=None):
+def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, store=None, alive_topk=False):
     """DMoE(x) of Eq. 1: sum over the alive chosen experts of f(x) times its
     renormalised weight.  experts is (W1, b1, W2, b2) stacked over experts or a
     callable e -> (W1_e, b1_e, W2_e, b2_e), all fp64.  only_experts restricts the
@@ -318,7 +343,7 @@ def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, s
     x = np.asarray(x, np.float64)
     T, D = x.shape
     N = M ** d
-    r = routing(x, Wg, bg, alive, d, M, k)
+    r = routing(x, Wg, bg, alive, d, M, k, alive_topk)
     counts, offsets, row_token, pos = dispatch(r["idx"], alive, N)
     get = _expert_getter(experts)
     rows = int(offsets[-1])

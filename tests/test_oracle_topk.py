@@ -210,3 +210,44 @@ def test_bf16_products_exact_in_fp64():
         for c in range(6):
             exact = sum(Fraction(float(x[t, j])) * Fraction(float(W[c, j])) for j in range(16))
             assert abs(Fraction(float(S[t, c])) - exact) <= abs(exact) * Fraction(1, 2 ** 50)
+
+
+# ------------------------------------------------------------------ TopK among alive experts
+
+def test_alive_topk_golden_six_experts():
+    """The App. C example: six active experts; the exact best among them is the
+    fixture's exact_active (which Algorithm 1's beam need not find)."""
+    kv = dict(read_golden("beam_appC_six_experts.txt"))
+    d, M, k = int(kv["d"][0]), int(kv["M"][0]), int(kv["k"][0])
+    S32 = _f32([[float(v) for v in kv["scores"]]])
+    alive = np.zeros(M ** d)
+    for item in kv["active"]:
+        p, suf = item.split(":")
+        for s_ in suf.split(","):
+            alive[int(p) * M + int(s_)] = 1
+    idx, g = O.topk_alive_bruteforce(S32, d, M, k, alive)
+    assert idx[0].tolist() == [int(v) for v in kv["exact_active_idx"]]
+    assert g[0].tolist() == [float(v) for v in kv["exact_active_g"]]
+
+
+@pytest.mark.parametrize("d,M", [(1, 6), (2, 4), (3, 3)])
+def test_alive_topk_reductions(d, M):
+    """All alive (or all dead): the plain TopK.  Alive experts always come first, in
+    the plain order; with fewer than k alive, the best dead ones follow, in order."""
+    rng = np.random.default_rng(7 * d + M)
+    N, T = M ** d, 30
+    S32 = _f32(rng.standard_normal((T, d * M)))
+    for k in sorted({1, 2, min(4, N), N}):
+        ref, rg = O.topk_bruteforce(S32, d, M, k)
+        for alive in (np.ones(N), np.zeros(N)):
+            idx, g = O.topk_alive_bruteforce(S32, d, M, k, alive)
+            np.testing.assert_array_equal(idx, ref)
+            np.testing.assert_array_equal(g, rg)
+        alive = (rng.random(N) < 0.5).astype(float)
+        alive[0] = 1.0
+        idx, _ = O.topk_alive_bruteforce(S32, d, M, k, alive)
+        full, _ = O.topk_bruteforce(S32, d, M, N)
+        for t in range(T):
+            order_live = [f for f in full[t] if alive[f]]
+            order_dead = [f for f in full[t] if not alive[f]]
+            assert idx[t].tolist() == (order_live + order_dead)[:k]
