@@ -156,6 +156,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--recompute", action="store_true",
                     help="backward regenerates h and a (dmoe_expert_ffn_bwd_recompute)")
+    ap.add_argument("--alive-topk", action="store_true",
+                    help="TopK among the alive experts only (DMOE_FLAG_ALIVE_TOPK)")
     ap.add_argument("--sgd", action="store_true",
                     help="backward updates the expert parameters in place (dmoe_expert_ffn_bwd_sgd, lr 1e-4)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -185,7 +187,9 @@ def main():
     dW1, db1 = torch.empty_like(W1), torch.empty_like(b1)
     dW2, db2 = torch.empty_like(W2), torch.empty_like(b2)
     dWg, dbg = torch.empty_like(Wg), torch.empty_like(bg)
-    L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, dh_aliases_h=False)
+    from paper_2002_04013_amd.abi import DMOE_FLAG_ALIVE_TOPK
+    L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, dh_aliases_h=False,
+                  flags=DMOE_FLAG_ALIVE_TOPK if args.alive_topk else 0)
     torch.cuda.synchronize()
     print(f"[bench] {wl.name}: inputs ready in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr,
           flush=True)
@@ -282,7 +286,8 @@ def main():
                    "grid": f"{'x'.join([str(wl.M)] * wl.d)}", "experts": wl.N, "k": wl.k,
                    "act": wl.act, "p_alive": wl.p_alive, "pass": "fwd+bwd" if wl.backward else "fwd",
                    "activations": "recomputed in backward" if args.recompute else "stored",
-                   "expert_update": "fused SGD in the backward" if args.sgd else "gradients returned"},
+                   "expert_update": "fused SGD in the backward" if args.sgd else "gradients returned",
+                   "topk": "among alive experts" if args.alive_topk else "all experts, dead ones weighted 0"},
         "roofline": roofline,
         "roofline_ffn_bwd": roof("ffn_bwd") if wl.backward else None,
         "gate_topk": roof("gate_topk"),

@@ -65,7 +65,13 @@ typedef struct {
  * bf16 gate scores with exact fp64 accumulation (the path it otherwise takes only
  * for tokens whose MFMA-computed decision is not certified).  Results are the same;
  * only the speed differs. */
-enum { DMOE_FLAG_GATE_EXACT = 1 };
+/* DMOE_FLAG_ALIVE_TOPK makes TopK choose among the alive experts only (the partially
+ * populated grid of App. C, where Algorithm 1 extends prefixes by active suffixes
+ * only): cells are ranked by (alive first, g descending, lower flat index) and the k
+ * first chosen, so dead experts are taken only when fewer than k are alive (they get
+ * weight 0).  Without it, TopK ranks every expert and dead chosen ones get weight 0.
+ * With it, every token's gate scores use exact fp64 accumulation. */
+enum { DMOE_FLAG_GATE_EXACT = 1, DMOE_FLAG_ALIVE_TOPK = 2 };
 
 /* Bytes of device workspace every entry point below needs for these dims
  * (one buffer of this size serves all of them; it may be reused between calls

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_PKG, "libdmoe.so")
 DMOE_F32, DMOE_BF16 = 0, 1
 DMOE_RELU, DMOE_GELU = 0, 1
 DMOE_FLAG_GATE_EXACT = 1
+DMOE_FLAG_ALIVE_TOPK = 2
 
 # every extern "C" symbol the header declares
 EXPORTS = (

@@ -11,7 +11,7 @@ int check_dims(const dmoe_dims* dims, Shape* s) {
   if (q.T < 0 || q.D <= 0 || q.H <= 0 || q.d < 1 || q.M < 1 || q.k < 1) return DMOE_EINVAL;
   if (q.dtype != DMOE_F32 && q.dtype != DMOE_BF16) return DMOE_EINVAL;
   if (q.act != DMOE_RELU && q.act != DMOE_GELU) return DMOE_EINVAL;
-  if (q.flags & ~DMOE_FLAG_GATE_EXACT) return DMOE_EINVAL;
+  if (q.flags & ~(DMOE_FLAG_GATE_EXACT | DMOE_FLAG_ALIVE_TOPK)) return DMOE_EINVAL;
   if (q.d > DMAX) return DMOE_EUNSUPPORTED;
   int64_t N = 1;
   for (int i = 0; i < q.d; ++i) {

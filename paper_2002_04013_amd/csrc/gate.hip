@@ -452,43 +452,68 @@ __global__ void __launch_bounds__(GM_NT) gate_topk_mfma(GateMfmaArgs ga) {
   }
 }
 
+// Alive-first ranking of cells: alive before dead, then total desc, then flat asc.
+// A top-KMAX list lives in three register arrays; comparisons are branch-free.
+__device__ __forceinline__ bool key_better(int al, double at, int af, int bl, double bt, int bf) {
+  return (al > bl) | ((al == bl) & ((at > bt) | ((at == bt) & (af < bf))));
+}
+__device__ __forceinline__ void key_insert(int (&kl)[KMAX], double (&kt)[KMAX], int (&kf)[KMAX], int l, double t,
+                                           int f) {
+#pragma unroll
+  for (int p = 0; p < KMAX; ++p) {
+    const bool sw = key_better(l, t, f, kl[p], kt[p], kf[p]);
+    const int ol = kl[p], of = kf[p];
+    const double ot = kt[p];
+    kl[p] = sw ? l : ol; kt[p] = sw ? t : ot; kf[p] = sw ? f : of;
+    l = sw ? ol : l; t = sw ? ot : t; f = sw ? of : f;
+  }
+}
+
 // Exact path for the queued tokens: fp64 scores S[c] = sum_k x_k W[c][k] + b[c], then the
-// same selection as the fp32 layers.  One block per token at a time (persistent over
-// the queue); thread (c, slice) sums a contiguous k-slice with four fp64 accumulators
-// over interleaved 8-element groups, and the slices are added in order.
+// selection.  One block per token at a time (persistent over the queue); thread
+// (c, slice) sums a contiguous k-slice with four fp64 accumulators over interleaved
+// 8-element groups, and the slices are added in order.
+// ALIVE: TopK among the alive experts: every cell of the grid is ranked by (alive
+// first, total desc, flat asc), the totals adding the d fp32 decision scores in fp64
+// in dimension order; each thread keeps the best k of its cells, and the lists are
+// merged across each wave by shuffles and across the waves by one thread.
+template <typename E, bool ALIVE>
 __global__ void __launch_bounds__(GX_NT) gate_exact_kernel(GateArgs a, const int32_t* queue) {
   __shared__ double s64[DM_MAX];
   __shared__ double part[GX_NT];
+  __shared__ int wl_l[GX_NT / 64][KMAX], wl_f[GX_NT / 64][KMAX];
+  __shared__ double wl_t[GX_NT / 64][KMAX];
   const int tid = threadIdx.x;
   const int dM = a.dM;
   const int n = queue[0];
-  const bf16* x = reinterpret_cast<const bf16*>(a.x);
-  const bf16* W = reinterpret_cast<const bf16*>(a.Wg);
-  const bf16* bg = reinterpret_cast<const bf16*>(a.bg);
+  const E* x = reinterpret_cast<const E*>(a.x);
+  const E* W = reinterpret_cast<const E*>(a.Wg);
+  const E* bg = reinterpret_cast<const E*>(a.bg);
+  constexpr int VEC = 16 / sizeof(E);
   const int S = GX_NT / dM;                                  // k-slices (dM <= DM_MAX = 128 -> S >= 2)
-  const int KS = (a.D / 32 + S - 1) / S * 32;                // k per slice, multiple of 32
+  const int KS = (a.D / (4 * VEC) + S - 1) / S * (4 * VEC);  // k per slice, multiple of 4 vectors
   const int c = tid % dM, sl = tid / dM;
   for (int qi = blockIdx.x; qi < n; qi += gridDim.x) {
     const int t = queue[GQ_HEAD + qi];
     double acc4[4] = {0.0, 0.0, 0.0, 0.0};
     if (sl < S) {
-      const bf16* xr = x + (int64_t)t * a.D;
-      const bf16* wr = W + (int64_t)c * a.D;
+      const E* xr = x + (int64_t)t * a.D;
+      const E* wr = W + (int64_t)c * a.D;
       const int k1 = min(a.D, (sl + 1) * KS);
-      for (int kk = sl * KS; kk < k1; kk += 32) {
+      for (int kk = sl * KS; kk < k1; kk += 4 * VEC) {
         uint4 xv[4], wv[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          xv[u] = *reinterpret_cast<const uint4*>(xr + kk + 8 * u);
-          wv[u] = *reinterpret_cast<const uint4*>(wr + kk + 8 * u);
+          xv[u] = *reinterpret_cast<const uint4*>(xr + kk + VEC * u);
+          wv[u] = *reinterpret_cast<const uint4*>(wr + kk + VEC * u);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          float xf[8], wf[8];
-          Vec<bf16>::unpack(xv[u], xf);
-          Vec<bf16>::unpack(wv[u], wf);
+          float xf[VEC], wf[VEC];
+          Vec<E>::unpack(xv[u], xf);
+          Vec<E>::unpack(wv[u], wf);
 #pragma unroll
-          for (int q = 0; q < 8; ++q) acc4[u] = fma((double)xf[q], (double)wf[q], acc4[u]);
+          for (int q = 0; q < VEC; ++q) acc4[u] = fma((double)xf[q], (double)wf[q], acc4[u]);
         }
       }
     }
@@ -497,15 +522,96 @@ __global__ void __launch_bounds__(GX_NT) gate_exact_kernel(GateArgs a, const int
     if (tid < dM) {
       double v = 0.0;
       for (int q = 0; q < S; ++q) v += part[q * dM + tid];
-      s64[tid] = v + (bg ? (double)bf2f(bg[tid]) : 0.0);
+      s64[tid] = v + (bg ? (double)ldf(bg + tid) : 0.0);
     }
     __syncthreads();
-    if (tid == 0)
-      select_token<false>(s64, nullptr, a.alive, a.d, a.M, a.k, a.N, 0.f, a.idx + (int64_t)t * a.k,
-                          a.w + (int64_t)t * a.k, a.g ? a.g + (int64_t)t * a.k : nullptr);
+    if constexpr (!ALIVE) {
+      if (tid == 0)
+        select_token<false>(s64, nullptr, a.alive, a.d, a.M, a.k, a.N, 0.f, a.idx + (int64_t)t * a.k,
+                            a.w + (int64_t)t * a.k, a.g ? a.g + (int64_t)t * a.k : nullptr);
+    } else {
+      int kl[KMAX], kf[KMAX];
+      double kt[KMAX];
+#pragma unroll
+      for (int p = 0; p < KMAX; ++p) { kl[p] = -1; kt[p] = -INFINITY; kf[p] = 0x7fffffff; }
+      for (int f = tid; f < a.N; f += GX_NT) {
+        int rem = f, u[DMAX];
+#pragma unroll
+        for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < a.d) { u[i] = rem % a.M; rem /= a.M; } }
+        double tot = 0.0;
+#pragma unroll
+        for (int i = 0; i < DMAX; ++i) if (i < a.d) tot += (double)(float)s64[i * a.M + u[i]];
+        const int live = a.alive == nullptr || a.alive[f] != 0 ? 1 : 0;
+        key_insert(kl, kt, kf, live, tot, f);
+      }
+      // merge across the wave: lane takes the partner's list at distance 32, 16, .., 1
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        int ol[KMAX], of[KMAX];
+        double ot[KMAX];
+#pragma unroll
+        for (int p = 0; p < KMAX; ++p) {
+          ol[p] = __shfl_xor(kl[p], off, 64);
+          ot[p] = __shfl_xor(kt[p], off, 64);
+          of[p] = __shfl_xor(kf[p], off, 64);
+        }
+#pragma unroll
+        for (int p = 0; p < KMAX; ++p) key_insert(kl, kt, kf, ol[p], ot[p], of[p]);
+      }
+      if ((tid & 63) == 0) {
+#pragma unroll
+        for (int p = 0; p < KMAX; ++p) { wl_l[tid >> 6][p] = kl[p]; wl_t[tid >> 6][p] = kt[p]; wl_f[tid >> 6][p] = kf[p]; }
+      }
+      __syncthreads();
+      if (tid == 0) {
+        for (int w = 1; w < GX_NT / 64; ++w)
+#pragma unroll
+          for (int p = 0; p < KMAX; ++p) key_insert(kl, kt, kf, wl_l[w][p], wl_t[w][p], wl_f[w][p]);
+        // Eq. 1 weights from the fp64 totals of the chosen experts, over the alive ones
+        double gx[KMAX];
+        double m = -1.0e308;
+        bool any = false;
+#pragma unroll
+        for (int j = 0; j < KMAX; ++j) {
+          gx[j] = 0.0;
+          if (j < a.k) {
+            int rem = kf[j], u[DMAX];
+#pragma unroll
+            for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < a.d) { u[i] = rem % a.M; rem /= a.M; } }
+            double tt = 0.0;
+#pragma unroll
+            for (int i = 0; i < DMAX; ++i) if (i < a.d) tt += s64[i * a.M + u[i]];
+            gx[j] = tt;
+            if (kl[j] > 0) { any = true; m = tt > m ? tt : m; }
+          }
+        }
+        float ex[KMAX];
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < KMAX; ++j) {
+          ex[j] = j < a.k && kl[j] > 0 ? expf((float)(gx[j] - m)) : 0.f;
+          sum += ex[j];
+        }
+#pragma unroll
+        for (int j = 0; j < KMAX; ++j) {
+          if (j < a.k) {
+            a.idx[(int64_t)t * a.k + j] = kf[j];
+            a.w[(int64_t)t * a.k + j] = any ? ex[j] / sum : 0.f;
+            if (a.g) a.g[(int64_t)t * a.k + j] = (float)gx[j];
+          }
+        }
+      }
+    }
     if (a.scores && tid < dM) a.scores[(int64_t)t * dM + tid] = (float)s64[tid];
     __syncthreads();
   }
+}
+
+// every token into the queue (the exact path for all of them)
+__global__ void gate_queue_all(int32_t* queue, int T) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) queue[0] = T;
+  if (i < T) queue[GQ_HEAD + i] = i;
 }
 
 static size_t gate_mfma_lds_bytes(int dM) {
@@ -621,6 +727,19 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
   if (!aligned16(x) || !aligned16(Wg)) return DMOE_EUNSUPPORTED;
   GateArgs a{x, Wg, bg, alive, idx, w, g, scores, (int)s.T, (int)s.D, s.d, s.M, s.k, (int)s.dM, (int)s.N};
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (s.flags & DMOE_FLAG_ALIVE_TOPK) {
+    // TopK among the alive experts: exact scores and a ranking of every cell
+    if (!ws) return DMOE_EINVAL;
+    if (!aligned16(ws)) return DMOE_EUNSUPPORTED;
+    int32_t* queue = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + workspace_layout(s).gq_off);
+    hipLaunchKernelGGL(gate_queue_all, dim3((unsigned)((s.T + 255) / 256)), dim3(256), 0, st, queue, (int)s.T);
+    const int xgrid = (int)std::min<int64_t>(s.T, 2048);
+    if (s.dtype == DMOE_BF16)
+      hipLaunchKernelGGL((gate_exact_kernel<bf16, true>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+    else
+      hipLaunchKernelGGL((gate_exact_kernel<float, true>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+    return launch_status();
+  }
   if (s.dtype == DMOE_BF16 && s.dM <= 3 * 32) {
     if (!ws) return DMOE_EINVAL;
     if (!aligned16(ws)) return DMOE_EUNSUPPORTED;
@@ -642,7 +761,7 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
     hipLaunchKernelGGL(kern, grid, dim3(GM_NT), lds, st, ga);
     // exact recomputation of the queued tokens: persistent blocks over the queue
     const int xgrid = (int)std::min<int64_t>(s.T, 1024);
-    hipLaunchKernelGGL(gate_exact_kernel, dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+    hipLaunchKernelGGL((gate_exact_kernel<bf16, false>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
   } else {
     // fp32, and bf16 with more than 96 gate columns: exact fp64 scores for every token
     const dim3 grid((unsigned)((s.T + GATE_TB - 1) / GATE_TB));

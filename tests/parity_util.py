@@ -70,13 +70,14 @@ def gpu_run(wl, inp, backward=True, dh_aliases_h=False, flags=0, recompute=False
     return {k: v.detach().cpu() for k, v in out.items()}
 
 
-def oracle_run(wl, inp, backward=True):
+def oracle_run(wl, inp, backward=True, alive_topk=False):
     f = {n: O.to64(v) for n, v in inp.items() if n != "alive"}
     alive = inp["alive"].cpu().numpy()
     ex = (f["W1"], f["b1"], f["W2"], f["b2"])
     # a bf16 layer keeps h, a, expert outputs and their row gradients in bf16
     store = O.round_bf16 if wl.dtype == "bf16" else None
-    fwd = O.layer_forward(f["x"], f["Wg"], f["bg"], ex, alive, wl.d, wl.M, wl.k, wl.act, store=store)
+    fwd = O.layer_forward(f["x"], f["Wg"], f["bg"], ex, alive, wl.d, wl.M, wl.k, wl.act, store=store,
+                          alive_topk=alive_topk)
     bwd = O.layer_backward(fwd, f["dy"], f["x"], f["Wg"], ex, alive, wl.d, wl.M, wl.k, wl.act,
                            store=store) if backward else None
     return fwd, bwd

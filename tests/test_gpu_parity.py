@@ -259,3 +259,28 @@ def test_sgd_backward(name):
         np.testing.assert_array_equal(got[~live], old[~live], n + " (experts without rows)")
         if n in ("W1", "W2"):   # the update is visible, not absorbed by the rounding
             assert np.median(np.abs(got[live] - old[live])) > 2 * np.median(_ulp(old[live], wl.dtype)), n
+
+
+@pytest.mark.parametrize("name", ["bf16_skew", "bf16_grid3d", "f32_grid4d", "few_alive"])
+def test_alive_topk(name):
+    """DMOE_FLAG_ALIVE_TOPK: TopK among the alive experts (dead ones only to fill up
+    when fewer than k respond), the whole layer forward and backward against the
+    oracle's topk_alive_bruteforce routing; the chosen set differs from the plain
+    TopK's on these partially alive grids."""
+    from paper_2002_04013_amd.abi import DMOE_FLAG_ALIVE_TOPK
+    wl = CASES.get(name) or Workload("few_alive", 30, T=160, D=64, H=64, d=2, M=8, k=4, dtype="bf16",
+                                     act="gelu", p_alive=0.05)
+    say(f"[parity] alive TopK {name}")
+    inp = make_inputs(wl, "cpu")
+    if name == "few_alive":
+        alive = torch.zeros(wl.N, dtype=torch.uint8)
+        alive[[3, 17, 40]] = 1                     # three alive experts, k = 4
+        inp["alive"] = alive
+    gpu = gpu_run(wl, inp, flags=DMOE_FLAG_ALIVE_TOPK)
+    fwd, bwd = oracle_run(wl, inp, alive_topk=True)
+    compare(wl, inp, gpu, fwd, bwd)
+    plain, _ = oracle_run(wl, inp, backward=False)
+    assert not np.array_equal(plain["idx"], fwd["idx"])
+    live = inp["alive"].numpy().astype(bool)
+    chosen_live = live[gpu["idx"].numpy()].sum(axis=1)
+    assert (chosen_live == min(wl.k, int(live.sum()))).all()
