@@ -174,7 +174,7 @@ int dmoe_expert_ffn_bwd(const dmoe_dims* dims, const int32_t* offsets, const int
                         void* db1, void* dW2, void* db2, void* ws, void* stream);
 
 /* The same backward with the forward's activations recomputed instead of kept
- * (gradient checkpointing, as the Runtime's Backward does, Sec. 3.3 and App. E: it
+ * (gradient checkpointing, as the Runtime's Backward does, Sec. 3.3 and App. D: it
  * runs the expert's forward again when the gradient arrives; about one third more
  * expert arithmetic, and h and a need not survive from the forward call):
  *   h, a = x_perm W1_e^T + b1_e, act(.)   recomputed into the scratch h and a [P_max, H]
