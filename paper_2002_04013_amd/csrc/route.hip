@@ -3,8 +3,9 @@
 //
 // Dispatch is a stable counting sort by expert, without atomics on row order:
 //   1. per block of DISP_CHUNK pairs, an LDS histogram of alive pairs per expert;
-//   2. one block turns the histograms into counts, offsets (exclusive scan) and
-//      each block's starting row per expert;
+//   2. the histograms become each block's starting row per expert relative to the
+//      expert's first row (a scan down each column), the counts, and the offsets
+//      (an exclusive scan of the counts);
 //   3. each block ranks its pairs within every expert in pair order (wave-wide
 //      rank by lane comparison, waves taken in order) and writes pos/row_token;
 //   4. each token's row of x is copied to its alive pairs' rows of x_perm.
@@ -30,25 +31,46 @@ dispatch_hist(const int32_t* idx, const uint8_t* alive, int P, int N, int32_t* b
   for (int e = threadIdx.x; e < N; e += RT_NT) out[e] = hist[e];
 }
 
-// One block of 1024 threads; thread q owns experts [q*EPT, (q+1)*EPT).
-__global__ void __launch_bounds__(1024)
-dispatch_scan(int32_t* block_hist, int nb, int N, int32_t* counts, int32_t* offsets) {
-  __shared__ int sums[1024];
-  const int q = threadIdx.x;
-  const int EPT = (N + 1023) / 1024;
-  const int e0 = min(N, q * EPT), e1 = min(N, e0 + EPT);
-  int mine = 0;
-  for (int e = e0; e < e1; ++e) {
-    int run = 0;
-    for (int b = 0; b < nb; ++b) {
+// 2a. Per expert, the exclusive prefix of its per-block counts over the blocks (in
+// place) and its total.  A block takes SCAN_E experts (one per lane, so every access
+// is a coalesced row segment) in SCAN_S slices of the block rows; slice sums meet in
+// LDS and each slice then rewrites its rows from its own starting value.
+constexpr int SCAN_E = 64, SCAN_S = 16;
+__global__ void __launch_bounds__(SCAN_E * SCAN_S)
+dispatch_scan_cols(int32_t* block_hist, int nb, int N, int32_t* counts) {
+  __shared__ int part[SCAN_S][SCAN_E];
+  const int el = threadIdx.x % SCAN_E, sl = threadIdx.x / SCAN_E;
+  const int e = blockIdx.x * SCAN_E + el;
+  const int per = (nb + SCAN_S - 1) / SCAN_S;
+  const int b0 = min(nb, sl * per), b1 = min(nb, b0 + per);
+  int sum = 0;
+  if (e < N)
+    for (int b = b0; b < b1; ++b) sum += block_hist[(int64_t)b * N + e];
+  part[sl][el] = sum;
+  __syncthreads();
+  int run = 0;
+  for (int q = 0; q < sl; ++q) run += part[q][el];
+  if (e < N) {
+    for (int b = b0; b < b1; ++b) {
       int32_t* h = block_hist + (int64_t)b * N + e;
       const int c = *h;
       *h = run;
       run += c;
     }
-    counts[e] = run;
-    mine += run;
+    if (sl == SCAN_S - 1) counts[e] = run;
   }
+}
+
+// 2b. offsets = exclusive scan of counts, offsets[N] = total (one block of 1024
+// threads; thread q owns experts [q*EPT, (q+1)*EPT)).
+__global__ void __launch_bounds__(1024)
+dispatch_scan_offsets(const int32_t* counts, int N, int32_t* offsets) {
+  __shared__ int sums[1024];
+  const int q = threadIdx.x;
+  const int EPT = (N + 1023) / 1024;
+  const int e0 = min(N, q * EPT), e1 = min(N, e0 + EPT);
+  int mine = 0;
+  for (int e = e0; e < e1; ++e) mine += counts[e];
   sums[q] = mine;
   __syncthreads();
   for (int o = 1; o < 1024; o <<= 1) {     // inclusive Hillis-Steele scan
@@ -60,7 +82,6 @@ dispatch_scan(int32_t* block_hist, int nb, int N, int32_t* counts, int32_t* offs
   int base = sums[q] - mine;
   for (int e = e0; e < e1; ++e) {
     offsets[e] = base;
-    for (int b = 0; b < nb; ++b) block_hist[(int64_t)b * N + e] += base;
     base += counts[e];
   }
   if (q == 1023) offsets[N] = sums[1023];
@@ -68,10 +89,10 @@ dispatch_scan(int32_t* block_hist, int nb, int N, int32_t* counts, int32_t* offs
 
 __global__ void __launch_bounds__(RT_NT)
 dispatch_scatter(const int32_t* idx, const uint8_t* alive, int P, int N, int k,
-                 const int32_t* block_hist, int32_t* pos, int32_t* row_token) {
+                 const int32_t* block_hist, const int32_t* offsets, int32_t* pos, int32_t* row_token) {
   extern __shared__ int base[];
   const int32_t* bh = block_hist + (int64_t)blockIdx.x * N;
-  for (int e = threadIdx.x; e < N; e += RT_NT) base[e] = bh[e];
+  for (int e = threadIdx.x; e < N; e += RT_NT) base[e] = offsets[e] + bh[e];
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int r = 0; r < DISP_CHUNK / RT_NT; ++r) {
@@ -257,10 +278,12 @@ extern "C" int dmoe_dispatch(const dmoe_dims* dims, const void* x, const int32_t
   const int nb = (int)L.disp_blocks;
   if (nb > 0)
     hipLaunchKernelGGL(dispatch_hist, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N, bh);
-  hipLaunchKernelGGL(dispatch_scan, dim3(1), dim3(1024), 0, st, bh, nb, N, counts, offsets);
+  hipLaunchKernelGGL(dispatch_scan_cols, dim3((N + SCAN_E - 1) / SCAN_E), dim3(SCAN_E * SCAN_S), 0, st, bh, nb,
+                     N, counts);
+  hipLaunchKernelGGL(dispatch_scan_offsets, dim3(1), dim3(1024), 0, st, counts, N, offsets);
   if (nb == 0) return launch_status();
   hipLaunchKernelGGL(dispatch_scatter, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N,
-                     s.k, bh, pos, row_token);
+                     s.k, bh, offsets, pos, row_token);
   const int64_t chunks = s.T * (s.D * (int64_t)s.esz / 16);
   const int grid = (int)std::min<int64_t>((chunks + RT_NT - 1) / RT_NT, 256 * 16);
   if (s.dtype == DMOE_BF16)
