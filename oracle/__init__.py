@@ -14,7 +14,9 @@ Neural Networks using Decentralized Mixture-of-Experts", arXiv 2002.04013):
   * grouping of (token, expert) pairs per expert (the Runtime batching of
     Sec. 3.3), the expert feed-forward blocks and the weighted sum of Eq. 1;
   * the backward pass of all of the above, and the gradient-descent update of an
-    expert's parameters that the Runtime's Backward applies (Sec. 3.3).
+    expert's parameters that the Runtime's Backward applies (Sec. 3.3);
+  * the feed-forward block expert of Sec. 4.1 with layer normalisation between its
+    linear layers (oracle.ffblock).
 
 Only tests/, __graft_entry__.smoke() and bench.py's CPU-baseline leg may import
 this package.  The product path never calls it, and it imports nothing from
@@ -27,11 +29,16 @@ from .dmoe import (
     dispatch, expert_forward, expert_backward, gate_backward, layer_forward,
     layer_backward, routing, chosen_totals, round_bf16, expert_forward_stored, round_f32, sgd_step,
 )
+from .ffblock import (
+    LN_EPS, PARAM_NAMES, layernorm_act_forward, layernorm_act_backward, ffblock_forward_stored,
+    ffblock_backward,
+)
 
 __all__ = [
     "to64", "gate_scores", "decision_scores", "flat_index", "uid_of", "cell_totals",
     "topk_bruteforce", "topk_beam", "topk_product_key", "mixture_weights", "act",
     "act_grad", "dispatch", "expert_forward", "expert_backward", "gate_backward",
     "layer_forward", "layer_backward", "routing", "chosen_totals", "round_bf16", "expert_forward_stored",
-    "round_f32", "sgd_step", "topk_alive_bruteforce",
+    "round_f32", "sgd_step", "topk_alive_bruteforce", "LN_EPS", "PARAM_NAMES", "layernorm_act_forward",
+    "layernorm_act_backward", "ffblock_forward_stored", "ffblock_backward",
 ]

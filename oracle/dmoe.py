@@ -330,7 +330,8 @@ def _expert_getter(experts):
     return lambda e: (W1[e], b1[e], W2[e], b2[e])
 
 
-def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, store=None, alive_topk=False):
+def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, store=None, alive_topk=False,
+                  expert="ffn"):
     """DMoE(x) of Eq. 1: sum over the alive chosen experts of f(x) times its
     renormalised weight.  experts is (W1, b1, W2, b2) stacked over experts or a
     callable e -> (W1_e, b1_e, W2_e, b2_e), all fp64.  only_experts restricts the
@@ -338,20 +339,39 @@ def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, s
     for tokens that use them).  Returns a dict with the routing, the dispatch,
     the per-row h, a, y_perm (expert-grouped order) and the layer output y.
     store (optional) rounds the tensors a bf16 layer keeps in bf16 (h, a and the
-    expert outputs); all arithmetic stays exact."""
+    expert outputs); all arithmetic stays exact.
+    expert="ffblock": the experts are the LayerNorm feed-forward blocks of Sec. 4.1
+    (oracle.ffblock); experts(e) then returns a dict of that expert's parameters and
+    the per-row tensors are h1, a1, mean1, rstd1, h2, a2, mean2, rstd2 instead of h, a."""
     store = store or _identity
     x = np.asarray(x, np.float64)
     T, D = x.shape
     N = M ** d
     r = routing(x, Wg, bg, alive, d, M, k, alive_topk)
     counts, offsets, row_token, pos = dispatch(r["idx"], alive, N)
-    get = _expert_getter(experts)
+    get = _expert_getter(experts) if expert == "ffn" else None
     rows = int(offsets[-1])
     h = a = None
     y_perm = np.full((rows, D), np.nan)
     hs, as_ = {}, {}
     todo = np.nonzero(counts)[0] if only_experts is None else \
         [e for e in only_experts if counts[e] > 0]
+    if expert == "ffblock":
+        from .ffblock import ffblock_forward_stored
+        per_row = {}
+        for e in todo:
+            lo, hi = offsets[e], offsets[e + 1]
+            fw = ffblock_forward_stored(x[row_token[lo:hi]], experts(e), kind, store)
+            y_perm[lo:hi] = fw.pop("y")
+            for name, v in fw.items():
+                if name not in per_row:
+                    per_row[name] = np.full((rows,) + v.shape[1:], np.nan)
+                per_row[name][lo:hi] = v
+        todo = []
+    elif expert != "ffn":
+        raise ValueError(expert)
+    else:
+        per_row = {}
     for e in todo:
         lo, hi = offsets[e], offsets[e + 1]
         W1, b1, W2, b2 = get(e)
@@ -371,7 +391,7 @@ def layer_forward(x, Wg, bg, experts, alive, d, M, k, kind, only_experts=None, s
         ok = p >= 0
         y[ok] += r["w"][ok, j][:, None] * y_perm[p[ok]]
     return dict(r, counts=counts, offsets=offsets, row_token=row_token, pos=pos,
-                h=h, a=a, y_perm=y_perm, y=y)
+                h=h, a=a, y_perm=y_perm, y=y, **per_row)
 
 
 def gate_backward(w, dw, idx, alive, x, Wg, d, M):
@@ -395,14 +415,17 @@ def gate_backward(w, dw, idx, alive, x, Wg, d, M):
     return dg, ds, ds @ np.asarray(Wg, np.float64), ds.T @ x, ds.sum(axis=0)
 
 
-def layer_backward(fwd, dy, x, Wg, experts, alive, d, M, k, kind, only_experts=None, store=None):
+def layer_backward(fwd, dy, x, Wg, experts, alive, d, M, k, kind, only_experts=None, store=None,
+                   expert="ffn"):
     """Gradients of <DMoE(x), dy> with respect to x, the gate and the experts.
 
     dw_tj = <dy_t, f_j(x_t)> for alive chosen experts; the expert f_j receives
     w_tj dy_t as its output gradient; dx gathers every expert's input gradient
     plus the gate's.  Expert gradients are returned only for experts that got
     rows (an expert with no rows has zero gradient).  store (optional) rounds the
-    tensors a bf16 layer keeps in bf16 (output gradients per row, dH, dX per row)."""
+    tensors a bf16 layer keeps in bf16 (output gradients per row, dH, dX per row).
+    expert="ffblock": the LayerNorm blocks of Sec. 4.1; expert_grads[e] is then a dict
+    keyed by the parameter names, and the row gradients dh2, dh1 are returned too."""
     store = store or _identity
     x = np.asarray(x, np.float64)
     dy = np.asarray(dy, np.float64)
@@ -418,11 +441,28 @@ def layer_backward(fwd, dy, x, Wg, experts, alive, d, M, k, kind, only_experts=N
         dw[ok, j] = np.einsum("td,td->t", dy[ok], y_perm[p[ok]])
         dy_perm[p[ok]] = store(w[ok, j][:, None] * dy[ok])
     dg, ds, dx_gate, dWg, dbg = gate_backward(w, dw, idx, alive, x, Wg, d, M)
-    get = _expert_getter(experts)
     dx_perm = np.full((y_perm.shape[0], D), np.nan)
     grads = {}
     todo = np.nonzero(counts)[0] if only_experts is None else \
         [e for e in only_experts if counts[e] > 0]
+    extra = {}
+    if expert == "ffblock":
+        from .ffblock import ffblock_backward
+        names = ("h1", "a1", "h2", "a2")
+        for e in todo:
+            lo, hi = offsets[e], offsets[e + 1]
+            fw = {n: fwd[n][lo:hi] for n in names}
+            bw = ffblock_backward(x[row_token[lo:hi]], fw, dy_perm[lo:hi], experts(e), kind, store)
+            dx_perm[lo:hi] = bw["dX"]
+            for n in ("dh2", "dh1"):
+                if n not in extra:
+                    extra[n] = np.full((y_perm.shape[0],) + bw[n].shape[1:], np.nan)
+                extra[n][lo:hi] = bw[n]
+            grads[e] = bw["grads"]
+        todo = []
+    elif expert != "ffn":
+        raise ValueError(expert)
+    get = _expert_getter(experts) if expert == "ffn" else None
     for e in todo:
         lo, hi = offsets[e], offsets[e + 1]
         W1, b1, W2, b2 = get(e)
@@ -437,4 +477,4 @@ def layer_backward(fwd, dy, x, Wg, experts, alive, d, M, k, kind, only_experts=N
         ok = p >= 0
         dx[ok] += dx_perm[p[ok]]
     return dict(dw=dw, dg=dg, ds=ds, dy_perm=dy_perm, dx_perm=dx_perm, dx=dx,
-                dWg=dWg, dbg=dbg, expert_grads=grads)
+                dWg=dWg, dbg=dbg, expert_grads=grads, **extra)
