@@ -10,7 +10,8 @@
  *   DMoE(x) = sum_{f in TopK(x)} f(x) exp(g(x,f)) / sum_{f' in TopK(x)} exp(g(x,f')),
  *   with experts that do not respond excluded and the remaining weights
  *   renormalised to sum to 1 (Sec. 3.2).
- * Each expert is the feed-forward block f(x) = W2 act(W1 x + b1) + b2 (Sec. 4.1).
+ * Each expert is the feed-forward block f(x) = W2 act(W1 x + b1) + b2 (Sec. 4.1), or the
+ * block with layer normalisation of the dmoe_expert_ffblock_* entry points below.
  *
  * Conventions shared by every entry point
  *   - Every array pointer is a DEVICE pointer, row-major, owned by the caller.
@@ -207,6 +208,76 @@ int dmoe_expert_ffn_bwd_sgd(const dmoe_dims* dims, const int32_t* offsets, const
 int dmoe_dispatch_bwd(const dmoe_dims* dims, const void* dx_perm, const int32_t* pos,
                       const int32_t* idx, const float* dg, const void* Wg, void* dx,
                       void* stream);
+
+/* ------------------------------------------------------------------------------
+ * The feed-forward block expert of Sec. 4.1: linear layers of widths D -> F -> F -> D
+ * with layer normalisation and the activation between them,
+ *   h1 = x W1^T + b1,  a1 = act(LN(h1; g1, be1)),
+ *   h2 = a1 W2^T + b2, a2 = act(LN(h2; g2, be2)),
+ *   y  = a2 W3^T + b3,
+ * LN(h; g, b) = g (h - mean(h)) / sqrt(var(h) + 1e-5) + b over the F features of a row
+ * (biased variance).  F = dims->H, D = dims->D, act = dims->act; F is at most 4096
+ * for bf16 and 2048 for fp32.  These entry points replace dmoe_expert_ffn_fwd/bwd
+ * for a layer whose experts are such blocks; gate, dispatch and combine are shared.
+ * ------------------------------------------------------------------------------ */
+
+/* The parameters of every expert, stacked over the N experts, in the layer dtype,
+ * row-major: W1 [N,F,D], b1 [N,F], g1 and be1 [N,F] (scale and shift of the first
+ * normalisation), W2 [N,F,F], b2 [N,F], g2 and be2 [N,F], W3 [N,D,F], b3 [N,D].
+ * The same struct carries their gradients (same shapes). */
+typedef struct {
+  void* W1; void* b1; void* g1; void* be1;
+  void* W2; void* b2; void* g2; void* be2;
+  void* W3; void* b3;
+} dmoe_ffblock_params;
+
+/* Per-row tensors the forward keeps for the backward (P_max rows each, in expert
+ * row order like x_perm): h1, a1, h2, a2 [P_max, F] in the layer dtype; st1, st2
+ * [P_max, 2] fp32 holding each row's (mean, 1/sqrt(var + 1e-5)) of h1 and h2. */
+typedef struct {
+  void* h1; void* a1; float* st1;
+  void* h2; void* a2; float* st2;
+} dmoe_ffblock_acts;
+
+/* Forward of the block experts on the expert-grouped rows (the Runtime's batched
+ * Forward, Sec. 3.3; the block of Sec. 4.1).  x_perm [P_max, D] and offsets [N+1]
+ * come from dmoe_dispatch; writes every buffer of *acts and y_perm [P_max, D] for
+ * the rows [0, offsets[N]).  Uses workspace. */
+int dmoe_expert_ffblock_fwd(const dmoe_dims* dims, const int32_t* offsets, const void* x_perm,
+                            const dmoe_ffblock_params* params, const dmoe_ffblock_acts* acts,
+                            void* y_perm, void* ws, void* stream);
+
+/* Backward of the block experts (the Runtime's Backward, Sec. 3.3): from dy_perm
+ * [P_max, D] (dmoe_combine_bwd) and the forward's *acts,
+ *   dW3 = dy^T a2, db3 = sum dy, da2 = dy W3,  g2 <- da2, then dh2 in place,
+ *   dg2, dbe2 and dh2 = the normalisation backward at h2,
+ *   dW2 = dh2^T a1, db2 = sum dh2, da1 = dh2 W2, g1 <- da1, then dh1 in place,
+ *   dW1 = dh1^T x_perm, db1 = sum dh1, dx_perm = dh1 W1,
+ * per expert over its rows.  g1 and g2 are caller-owned [P_max, F] buffers in the
+ * layer dtype that end holding dh1 and dh2.  grads receives every parameter gradient;
+ * experts with no rows keep the caller's contents.  No output may alias an input.
+ * Uses workspace. */
+int dmoe_expert_ffblock_bwd(const dmoe_dims* dims, const int32_t* offsets, const void* x_perm,
+                            const dmoe_ffblock_params* params, const dmoe_ffblock_acts* acts,
+                            const void* dy_perm, void* g1, void* g2, void* dx_perm,
+                            const dmoe_ffblock_params* grads, void* ws, void* stream);
+
+/* One normalisation step of the block on its own (Sec. 4.1): for each row r of h
+ * [P_max, F] (rows [0, offsets[N]), F = dims->H) owned by expert e,
+ *   stats[r] = (mean, rstd) fp32, a[r] = act(gamma[e] (h[r] - mean) rstd + beta[e]),
+ * gamma and beta [N, F].  No workspace. */
+int dmoe_ln_act_fwd(const dmoe_dims* dims, const int32_t* offsets, const void* h, const void* gamma,
+                    const void* beta, void* a, float* stats, void* stream);
+
+/* Backward of dmoe_ln_act_fwd given da [P_max, F] and the forward's stats:
+ *   n = (h - mean) rstd, dz = da act'(gamma n + beta), dn = dz gamma,
+ *   dh = rstd (dn - mean_f(dn) - n mean_f(dn n)),
+ *   dgamma[e] = sum over e's rows of dz n, dbeta[e] = sum over e's rows of dz.
+ * dh may alias da (the scale and shift gradients are taken before dh is written);
+ * experts with no rows keep the caller's dgamma, dbeta.  No workspace. */
+int dmoe_ln_act_bwd(const dmoe_dims* dims, const int32_t* offsets, const void* h, const float* stats,
+                    const void* gamma, const void* beta, const void* da, void* dh, void* dgamma,
+                    void* dbeta, void* stream);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,12 @@ EXPORTS = (
     "dmoe_workspace_bytes", "dmoe_strerror", "dmoe_gate_topk", "dmoe_dispatch",
     "dmoe_expert_ffn_fwd", "dmoe_combine", "dmoe_combine_bwd", "dmoe_gate_topk_bwd",
     "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd", "dmoe_expert_ffn_bwd_recompute", "dmoe_expert_ffn_bwd_sgd",
+    "dmoe_expert_ffblock_fwd", "dmoe_expert_ffblock_bwd", "dmoe_ln_act_fwd", "dmoe_ln_act_bwd",
 )
+
+# parameters of the feed-forward block expert, in dmoe_ffblock_params order
+FFBLOCK_PARAMS = ("W1", "b1", "g1", "be1", "W2", "b2", "g2", "be2", "W3", "b3")
+FFBLOCK_ACTS = ("h1", "a1", "st1", "h2", "a2", "st2")
 
 
 class DmoeError(RuntimeError):
@@ -34,6 +39,14 @@ class Dims(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int64), ("D", ctypes.c_int64), ("H", ctypes.c_int64),
                 ("d", ctypes.c_int32), ("M", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("flags", ctypes.c_int32)]
+
+
+class FFBlockParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in FFBLOCK_PARAMS]
+
+
+class FFBlockActs(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in FFBLOCK_ACTS]
 
 
 def make_dims(T, D, H, d, M, k, dtype="bf16", act="gelu", flags=0):
@@ -68,6 +81,13 @@ def load(path=LIB_PATH):
         "dmoe_dispatch_bwd": (ctypes.c_int, [pd] + [_P] * 7),
         "dmoe_expert_ffn_bwd_recompute": (ctypes.c_int, [pd] + [_P] * 16),
         "dmoe_expert_ffn_bwd_sgd": (ctypes.c_int, [pd] + [_P] * 10 + [ctypes.c_float] + [_P] * 4),
+        "dmoe_expert_ffblock_fwd": (ctypes.c_int, [pd, _P, _P, ctypes.POINTER(FFBlockParams),
+                                                   ctypes.POINTER(FFBlockActs), _P, _P, _P]),
+        "dmoe_expert_ffblock_bwd": (ctypes.c_int, [pd, _P, _P, ctypes.POINTER(FFBlockParams),
+                                                   ctypes.POINTER(FFBlockActs), _P, _P, _P, _P,
+                                                   ctypes.POINTER(FFBlockParams), _P, _P]),
+        "dmoe_ln_act_fwd": (ctypes.c_int, [pd] + [_P] * 7),
+        "dmoe_ln_act_bwd": (ctypes.c_int, [pd] + [_P] * 10),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -169,3 +189,40 @@ def dmoe_expert_ffn_bwd_sgd(dims, offsets, counts, x_perm, h, a, dy_perm, W1, b1
                                           _ptr(a), _ptr(dy_perm), _ptr(W1), _ptr(b1), _ptr(W2), _ptr(b2),
                                           ctypes.c_float(lr), _ptr(dh), _ptr(dx_perm), _ptr(ws), _stream(stream)),
            "dmoe_expert_ffn_bwd_sgd")
+
+
+def _block_params(t):
+    """dict name -> device tensor (FFBLOCK_PARAMS) as a dmoe_ffblock_params struct."""
+    return FFBlockParams(*[_ptr(t[n]) for n in FFBLOCK_PARAMS])
+
+
+def _block_acts(t):
+    return FFBlockActs(*[_ptr(t[n]) for n in FFBLOCK_ACTS])
+
+
+def dmoe_expert_ffblock_fwd(dims, offsets, x_perm, params, acts, y_perm, ws, stream=None):
+    """params: dict of the block parameters (FFBLOCK_PARAMS); acts: dict of the kept
+    per-row tensors (FFBLOCK_ACTS)."""
+    p, a = _block_params(params), _block_acts(acts)
+    _check(load().dmoe_expert_ffblock_fwd(ctypes.byref(dims), _ptr(offsets), _ptr(x_perm), ctypes.byref(p),
+                                          ctypes.byref(a), _ptr(y_perm), _ptr(ws), _stream(stream)),
+           "dmoe_expert_ffblock_fwd")
+
+
+def dmoe_expert_ffblock_bwd(dims, offsets, x_perm, params, acts, dy_perm, g1, g2, dx_perm, grads, ws, stream=None):
+    """grads: dict of gradient tensors with the parameters' names and shapes."""
+    p, a, g = _block_params(params), _block_acts(acts), _block_params(grads)
+    _check(load().dmoe_expert_ffblock_bwd(ctypes.byref(dims), _ptr(offsets), _ptr(x_perm), ctypes.byref(p),
+                                          ctypes.byref(a), _ptr(dy_perm), _ptr(g1), _ptr(g2), _ptr(dx_perm),
+                                          ctypes.byref(g), _ptr(ws), _stream(stream)), "dmoe_expert_ffblock_bwd")
+
+
+def dmoe_ln_act_fwd(dims, offsets, h, gamma, beta, a, stats, stream=None):
+    _check(load().dmoe_ln_act_fwd(ctypes.byref(dims), _ptr(offsets), _ptr(h), _ptr(gamma), _ptr(beta), _ptr(a),
+                                  _ptr(stats), _stream(stream)), "dmoe_ln_act_fwd")
+
+
+def dmoe_ln_act_bwd(dims, offsets, h, stats, gamma, beta, da, dh, dgamma, dbeta, stream=None):
+    _check(load().dmoe_ln_act_bwd(ctypes.byref(dims), _ptr(offsets), _ptr(h), _ptr(stats), _ptr(gamma),
+                                  _ptr(beta), _ptr(da), _ptr(dh), _ptr(dgamma), _ptr(dbeta), _stream(stream)),
+           "dmoe_ln_act_bwd")

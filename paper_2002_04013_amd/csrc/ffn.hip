@@ -2,154 +2,9 @@
 // Forward and Backward of Sec. 3.3), as grouped GEMMs on MFMA.
 #include <algorithm>
 
-#include "common.hpp"
-#include "gemm.hpp"
-#include "gemm2.hpp"
+#include "grouped.hpp"
 
 namespace dmoe {
-
-// Tile plan of one FFN call, from the expert row offsets:
-//   plan[e]         = sum over experts before e of ceil(rows / BM)   (GROUP_M m-tiles)
-//   plan[N + 1 + e] = number of experts before e that have rows      (GROUP_K experts)
-// A GEMM with NT n-tiles (GROUP_M) or MT*NT tiles per expert (GROUP_K) scales these.
-__global__ void __launch_bounds__(1024)
-tile_plan(const int32_t* offsets, int N, int BM, int32_t* plan) {
-  __shared__ int s_mt[1024], s_ac[1024];
-  const int q = threadIdx.x;
-  const int EPT = (N + 1023) / 1024;
-  const int e0 = min(N, q * EPT), e1 = min(N, e0 + EPT);
-  int mt = 0, ac = 0;
-  for (int e = e0; e < e1; ++e) {
-    const int c = offsets[e + 1] - offsets[e];
-    mt += (c + BM - 1) / BM;
-    ac += c > 0;
-  }
-  s_mt[q] = mt;
-  s_ac[q] = ac;
-  __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {
-    const int a = q >= o ? s_mt[q - o] : 0, b = q >= o ? s_ac[q - o] : 0;
-    __syncthreads();
-    s_mt[q] += a;
-    s_ac[q] += b;
-    __syncthreads();
-  }
-  int bm = s_mt[q] - mt, ba = s_ac[q] - ac;
-  int32_t* act = plan + N + 1;
-  for (int e = e0; e < e1; ++e) {
-    plan[e] = bm;
-    act[e] = ba;
-    const int c = offsets[e + 1] - offsets[e];
-    bm += (c + BM - 1) / BM;
-    ba += c > 0;
-  }
-  if (q == 1023) {
-    plan[N] = s_mt[1023];
-    act[N] = s_ac[1023];
-  }
-}
-
-// out[e][c] = sum of rows [offsets[e], offsets[e+1]) of X[:, c]  (bias gradients);
-// experts without rows are skipped (their slots are left untouched).
-// out[e][c] = sum of rows [offsets[e], offsets[e+1]) of column c (experts without rows
-// are left untouched); SGD: out[e][c] -= lr * that sum (out holds the parameters).
-template <typename E, bool SGD = false>
-__global__ void __launch_bounds__(256)
-segment_colsum(const E* X, int64_t ld, const int32_t* offsets, int ncols, E* out, float lr = 0.f) {
-  constexpr int VEC = 16 / sizeof(E);
-  const int e = blockIdx.y;
-  const int r0 = offsets[e], r1 = offsets[e + 1];
-  if (r1 == r0) return;
-  const int c = (blockIdx.x * 256 + threadIdx.x) * VEC;
-  if (c >= ncols) return;
-  float acc[VEC];
-#pragma unroll
-  for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
-  for (int r = r0; r < r1; ++r) {
-    float v[VEC];
-    Vec<E>::unpack(*reinterpret_cast<const uint4*>(X + (int64_t)r * ld + c), v);
-#pragma unroll
-    for (int i = 0; i < VEC; ++i) acc[i] += v[i];
-  }
-  uint4* op = reinterpret_cast<uint4*>(out + (int64_t)e * ncols + c);
-  if constexpr (SGD) {
-    float w[VEC];
-    Vec<E>::unpack(*op, w);
-#pragma unroll
-    for (int i = 0; i < VEC; ++i) acc[i] = w[i] - lr * acc[i];
-  }
-  *op = Vec<E>::pack(acc);
-}
-
-static int device_cus() {
-  static int cus[64] = {0};
-  int dev = 0;
-  hipGetDevice(&dev);
-  if (dev < 0 || dev >= 64) return 256;
-  if (!cus[dev]) {
-    int v = 0;
-    hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev);
-    cus[dev] = v > 0 ? v : 256;
-  }
-  return cus[dev];
-}
-
-template <typename E, int GM, bool B_KC, int EPI, int BM, int BN, int BK, int WM, int WN>
-static void run_gemm(GemmArgs<E> p, int64_t tiles_ub, hipStream_t st) {
-  if (tiles_ub <= 0) return;
-  auto kern = grouped_gemm<E, GM, B_KC, EPI, BM, BN, BK, WM, WN>;
-  constexpr int NT = 64 * WM * WN;
-  const size_t lds = gemm_lds_bytes<E, BM, BN, BK, WM, WN>();
-  static int per_cu = 0;
-  if (!per_cu) {
-    int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, NT, lds) != hipSuccess || nb < 1) nb = 1;
-    per_cu = nb;
-  }
-  const int64_t resident = (int64_t)per_cu * device_cus();
-  const int grid = (int)std::min<int64_t>(tiles_ub, resident);
-  p.chunked = grid >= 8;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
-}
-
-// gfx950 bf16 path: direct-to-LDS multi-stage GEMM (gemm2.hpp)
-template <int GM, bool AT, bool BT, int EPI, int BM, int BN, int WM, int WN, int ST, int BK>
-static void run_gemm2(GemmArgs<bf16> p, int64_t tiles_ub, hipStream_t st) {
-  if (tiles_ub <= 0) return;
-  auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1, BK>;
-  constexpr int NT = 64 * WM * WN;
-  const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT, BK>();
-  static int per_cu = 0;
-  if (!per_cu) {
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, NT, lds) != hipSuccess || nb < 1) nb = 1;
-    (void)hipGetLastError();
-    per_cu = nb;
-  }
-  const int64_t resident = (int64_t)per_cu * device_cus();
-  const int grid = (int)std::min<int64_t>(tiles_ub, resident);
-  p.chunked = grid >= 8;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
-}
-
-template <typename E>
-static GemmArgs<E> args_m(const int32_t* offsets, const int32_t* tpre, int scale, int N) {
-  GemmArgs<E> p{};
-  p.offsets = offsets; p.tprefix = tpre; p.tscale = scale; p.groups = N;
-  return p;
-}
-
-// fp32 tile shapes (register-staged MFMA GEMM of gemm.hpp).
-struct CfgF32    { static constexpr int BM = 32, BN = 64, BK = 32, WM = 1, WN = 2; };
-struct CfgDWF32  { static constexpr int BM = 64, BN = 64, BK = 32, WM = 2, WN = 2; };
-
-// bf16 tile shapes of the gemm2 path: many rows per expert -> 256x256 tiles, 8 waves,
-// 64-deep k, 2 stages (best of the measured shapes at the wide workload for all three
-// operand layouts); few rows -> 32x256 tiles, 4 waves, 4 stages (weight streaming).
-struct G2Fat    { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
-struct G2Skinny { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4, BK = 64; };
-struct G2DW     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
 
 template <typename C>
 static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, const bf16* W1,
@@ -394,8 +249,6 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   hipLaunchKernelGGL((segment_colsum<E, SGD>), dim3((unsigned)((D / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
                      st, dyp, (int64_t)D, offsets, D, db2, lr);
 }
-
-static bool use_fat(const Shape& s) { return s.P >= (int64_t)96 * s.N; }
 
 template <typename E, typename C>
 static void ffn_up_cfg(const Shape& s, const int32_t* offsets, const E* xp, const E* W1, const E* b1, E* h, E* a,

@@ -5,6 +5,7 @@ torch.autograd on a dense fp64 reformulation of the layer (written here with
 torch ops only), central finite differences and invariants of Eq. 1.
 """
 import math
+import zlib
 
 import numpy as np
 import pytest
@@ -213,7 +214,7 @@ def _torch_dense_layer(P, kind):
 @pytest.mark.parametrize("shape", [dict(d=2, M=3, k=3, p=0.8), dict(d=3, M=2, k=4, p=0.6),
                                    dict(d=1, M=6, k=6, p=1.0), dict(d=2, M=4, k=2, p=0.3)])
 def test_layer_vs_torch_autograd(kind, shape):
-    P = _problem(seed=hash((kind, tuple(shape.items()))) % 1000, **shape)
+    P = _problem(seed=zlib.crc32(repr((kind, sorted(shape.items()))).encode()) % 1000, **shape)
     fwd, bwd = _run(P, kind)
     idx, w, y, grads = _torch_dense_layer(P, kind)
     np.testing.assert_array_equal(fwd["idx"], idx)

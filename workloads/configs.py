@@ -1,8 +1,9 @@
-"""The five DMoE workloads, named by what they are.
+"""The DMoE workloads, named by what they are.
 
 Shapes follow the paper's Transformer-style experts (d_model 1024, FFN 4096,
-GELU; top-4 routing; a 10% expert failure rate) and a wide layer that replaces
-a Transformer FFN (d_model 4096, FFN 16384).
+GELU; top-4 routing; a 10% expert failure rate), a wide layer that replaces
+a Transformer FFN (d_model 4096, FFN 16384), and the paper's feed-forward block
+experts with layer normalisation (1024 -> 4096 -> 4096 -> 1024, ReLU).
 """
 from dataclasses import dataclass, replace
 
@@ -24,6 +25,8 @@ class Workload:
     skew_rows: int = 0   # per grid dim, this many indices get a further x4 gate scale
     backward: bool = True
     seed: int = 0
+    expert: str = "ffn"  # "ffn": Linear-act-Linear; "ffblock": the LayerNorm block of Sec. 4.1
+    ln_init: str = "standard"  # ffblock: LayerNorm scale 1, shift 0; "split": scale 1/2, shift +-3
 
     @property
     def N(self) -> int:
@@ -55,6 +58,11 @@ WORKLOADS = {
     # Wide layer: 32768 tokens (16 x 2048), d_model 4096, 16x16 grid, 4096->16384->4096.
     "wide": Workload("wide", 4, T=32768, D=4096, H=16384, d=2, M=16, k=4,
                      dtype="bf16", act="gelu"),
+    # The paper's own expert (Sec. 4.1): feed-forward blocks 1024->4096->4096->1024 with
+    # LayerNorm and ReLU between the layers, batches of 2048 rows per block: 131072
+    # tokens, 16x16 grid (256 blocks), top-4 -> 2048 rows per expert on average.
+    "ffblock": Workload("ffblock", 5, T=131072, D=1024, H=4096, d=2, M=16, k=4,
+                        dtype="bf16", act="relu", expert="ffblock"),
 }
 
 

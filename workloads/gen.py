@@ -13,7 +13,7 @@ from .configs import Workload
 _MASK64 = (1 << 64) - 1
 
 # tensor ids
-_X, _WG, _BG, _W1, _B1, _W2, _B2, _ALIVE, _DY, _SKEW = range(10)
+_X, _WG, _BG, _W1, _B1, _W2, _B2, _ALIVE, _DY, _SKEW, _W3, _B3, _LN = range(13)
 
 
 def _mix(z: int) -> int:
@@ -122,3 +122,52 @@ def make_inputs(wl: Workload, device="cpu", identical_experts=False):
     W1, b1, W2, b2 = make_experts(wl, device, identical=identical_experts)
     return dict(x=make_x(wl, device), Wg=Wg, bg=bg, alive=make_alive(wl, device),
                 W1=W1, b1=b1, W2=W2, b2=b2, dy=make_dy(wl, device))
+
+
+# ---------------------------------------------------------------- block experts
+
+BLOCK_PARAMS = ("W1", "b1", "g1", "be1", "W2", "b2", "g2", "be2", "W3", "b3")
+
+
+def make_block_expert(wl: Workload, e: int, device="cpu"):
+    """Parameters of feed-forward block expert e (hidden width F = wl.H), nn.Linear and
+    nn.LayerNorm layouts: W1 [F,D], b1 [F] ~ N(0, 1/D); W2 [F,F], b2 [F] ~ N(0, 1/F);
+    W3 [D,F], b3 [D] ~ N(0, 1/F); LayerNorm scale g and shift be [F] at 1 and 0
+    (ln_init "standard"), or scale 1/2 and shift +3 or -3 by a seeded sign per feature
+    ("split": every normalised value lands at least 1/2 away from the activation's kink
+    for |n| < 5)."""
+    D, F = wl.D, wl.H
+    s1, s2 = D ** -0.5, F ** -0.5
+    dt = storage_dtype(wl)
+    p = dict(W1=_randn((F, D), s1, wl, _W1, e, device), b1=_randn((F,), s1, wl, _B1, e, device),
+             W2=_randn((F, F), s2, wl, _W2, e, device), b2=_randn((F,), s2, wl, _B2, e, device),
+             W3=_randn((D, F), s2, wl, _W3, e, device), b3=_randn((D,), s2, wl, _B3, e, device))
+    for i, (gn, bn) in enumerate((("g1", "be1"), ("g2", "be2"))):
+        if wl.ln_init == "standard":
+            p[gn] = torch.ones(F, dtype=dt, device=device)
+            p[bn] = torch.zeros(F, dtype=dt, device=device)
+        elif wl.ln_init == "split":
+            g = _gen("cpu", tensor_seed(wl.seed, wl.cfg_id, _LN, 2 * e + i))
+            sign = torch.randint(0, 2, (F,), generator=g).to(torch.float32) * 2 - 1
+            p[gn] = torch.full((F,), 0.5, dtype=dt, device=device)
+            p[bn] = (3.0 * sign).to(dt).to(device)
+        else:
+            raise ValueError(wl.ln_init)
+    return p
+
+
+def make_block_experts(wl: Workload, device="cpu"):
+    """Every block expert's parameters stacked over experts (dict keyed by BLOCK_PARAMS)."""
+    one = make_block_expert(wl, 0, device)
+    out = {n: torch.empty((wl.N,) + tuple(v.shape), dtype=v.dtype, device=device) for n, v in one.items()}
+    for e in range(wl.N):
+        p = one if e == 0 else make_block_expert(wl, e, device)
+        for n in BLOCK_PARAMS:
+            out[n][e].copy_(p[n])
+    return out
+
+
+def make_block_inputs(wl: Workload, device="cpu"):
+    Wg, bg = make_gate(wl, device)
+    return dict(x=make_x(wl, device), Wg=Wg, bg=bg, alive=make_alive(wl, device), dy=make_dy(wl, device),
+                params=make_block_experts(wl, device))
