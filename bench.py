@@ -54,6 +54,26 @@ def algorithmic(wl, counts, recompute=False, sgd=False):
     return out
 
 
+def algorithmic_block(wl, counts):
+    """Algorithmic bytes and flops of the block-expert calls (Linear, LayerNorm+act,
+    Linear, LayerNorm+act, Linear per expert): each weight read once per pass (twice in
+    the backward: data and weight gradients) and each gradient written once; every
+    row tensor read or written once per step that uses it."""
+    e = 2 if wl.dtype == "bf16" else 4
+    D, F = wl.D, wl.H
+    rows = int(sum(counts))
+    touched = int(sum(1 for c in counts if c > 0))
+    wbytes = touched * (2 * D * F + F * F + 6 * F + D) * e
+    flops = 2 * rows * F * (2 * D + F)
+    # fwd rows: GEMM1 x->h1, LN1 h1->a1 (+stats), GEMM2 a1->h2, LN2 h2->a2, GEMM3 a2->y
+    fwd_rows = rows * ((2 * D + 8 * F) * e + 16)
+    # bwd rows: dW3 (dy, a2), da2 (dy -> g2), db3 (dy), LN2 bwd (g2, h2 twice; g2 out),
+    # db2, dW2 (g2, a1), da1 (g2 -> g1), LN1 bwd, db1, dW1 (g1, x), dx (g1 -> dx)
+    bwd_rows = rows * ((5 * D + 21 * F) * e + 32)
+    return {"ffn_fwd": dict(bytes=wbytes + fwd_rows, flops=flops),
+            "ffn_bwd": dict(bytes=3 * wbytes + bwd_rows, flops=2 * flops)}
+
+
 def cpu_baseline(wl, inp, counts, budget_s=12.0):
     """The oracle, as it stands, on a bounded sample of the same workload: routing
     (gate, TopK, weights), dispatch and the gate backward for every token, then the
@@ -84,12 +104,19 @@ def cpu_baseline(wl, inp, counts, budget_s=12.0):
     rng.shuffle(live)
     t_exp, pairs, used = 0.0, 0, 0
     for e in live:
-        W1, b1, W2, b2 = (O.to64(inp[n][e]) for n in ("W1", "b1", "W2", "b2"))   # not timed
         rows = row_token[off[e]:off[e + 1]]
-        t1 = time.perf_counter()
-        X = x[rows]
-        h, a, y = O.expert_forward(X, W1, b1, W2, b2, wl.act)
-        O.expert_backward(X, h, a, dy[rows], W1, W2, wl.act)
+        if wl.expert == "ffblock":
+            prm = {n: O.to64(v[e]) for n, v in inp["params"].items()}                # not timed
+            t1 = time.perf_counter()
+            X = x[rows]
+            fw = O.ffblock_forward_stored(X, prm, wl.act)
+            O.ffblock_backward(X, fw, dy[rows], prm, wl.act)
+        else:
+            W1, b1, W2, b2 = (O.to64(inp[n][e]) for n in ("W1", "b1", "W2", "b2"))   # not timed
+            t1 = time.perf_counter()
+            X = x[rows]
+            h, a, y = O.expert_forward(X, W1, b1, W2, b2, wl.act)
+            O.expert_backward(X, h, a, dy[rows], W1, W2, wl.act)
         t_exp += time.perf_counter() - t1
         pairs += len(rows)
         used += 1
@@ -173,23 +200,35 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2002_04013_amd import DMoELayer
-    from workloads import get_workload, make_alive, make_dy, make_experts, make_gate, make_x
+    from paper_2002_04013_amd import DMoEBlockLayer, DMoELayer
+    from workloads import (get_workload, make_alive, make_block_experts, make_dy, make_experts, make_gate,
+                           make_x)
 
     wl = get_workload(args.workload)
+    block = wl.expert == "ffblock"
+    if block and (args.recompute or args.sgd):
+        print("bench.py: --recompute and --sgd apply to the Linear-act-Linear experts only", file=sys.stderr)
+        sys.exit(2)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     t_gen = time.perf_counter()
     Wg, bg = make_gate(wl, dev)
     inp = dict(x=make_x(wl, dev), dy=make_dy(wl, dev), Wg=Wg, bg=bg, alive=make_alive(wl, dev))
-    W1, b1, W2, b2 = make_experts(wl, dev)
-    inp.update(W1=W1, b1=b1, W2=W2, b2=b2)
-    dW1, db1 = torch.empty_like(W1), torch.empty_like(b1)
-    dW2, db2 = torch.empty_like(W2), torch.empty_like(b2)
     dWg, dbg = torch.empty_like(Wg), torch.empty_like(bg)
     from paper_2002_04013_amd.abi import DMOE_FLAG_ALIVE_TOPK
-    L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, dh_aliases_h=False,
-                  flags=DMOE_FLAG_ALIVE_TOPK if args.alive_topk else 0)
+    flags = DMOE_FLAG_ALIVE_TOPK if args.alive_topk else 0
+    if block:
+        prm = make_block_experts(wl, dev)
+        inp["params"] = prm
+        grads = {n: torch.empty_like(v) for n, v in prm.items()}
+        L = DMoEBlockLayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, flags=flags)
+    else:
+        W1, b1, W2, b2 = make_experts(wl, dev)
+        inp.update(W1=W1, b1=b1, W2=W2, b2=b2)
+        dW1, db1 = torch.empty_like(W1), torch.empty_like(b1)
+        dW2, db2 = torch.empty_like(W2), torch.empty_like(b2)
+        L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, dh_aliases_h=False,
+                      flags=flags)
     torch.cuda.synchronize()
     print(f"[bench] {wl.name}: inputs ready in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr,
           flush=True)
@@ -204,14 +243,18 @@ def main():
             ("gate_topk", lambda: abi.dmoe_gate_topk(Dm, x, Wg, bg, alive, L.idx, L.w, None, None, L.ws)),
             ("dispatch", lambda: abi.dmoe_dispatch(Dm, x, L.idx, alive, L.counts, L.offsets, L.row_token,
                                                    L.pos, L.x_perm, L.ws)),
-            ("ffn_fwd", lambda: abi.dmoe_expert_ffn_fwd(Dm, L.offsets, L.x_perm, W1, b1, W2, b2, L.h, L.a,
-                                                        L.y_perm, L.ws)),
+            ("ffn_fwd", (lambda: abi.dmoe_expert_ffblock_fwd(Dm, L.offsets, L.x_perm, prm, L.acts, L.y_perm,
+                                                             L.ws)) if block else
+             (lambda: abi.dmoe_expert_ffn_fwd(Dm, L.offsets, L.x_perm, W1, b1, W2, b2, L.h, L.a,
+                                              L.y_perm, L.ws))),
             ("combine", lambda: abi.dmoe_combine(Dm, L.y_perm, L.pos, L.w, L.y)),
             ("combine_bwd", lambda: abi.dmoe_combine_bwd(Dm, inp["dy"], L.y_perm, L.pos, L.w, L.dy_perm,
                                                          L.dw)),
             ("gate_topk_bwd", lambda: abi.dmoe_gate_topk_bwd(Dm, x, L.idx, L.w, L.dw, alive, L.dg, dWg, dbg,
                                                              L.ws)),
-            ("ffn_bwd", (lambda: abi.dmoe_expert_ffn_bwd_sgd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
+            ("ffn_bwd", (lambda: abi.dmoe_expert_ffblock_bwd(Dm, L.offsets, L.x_perm, prm, L.acts, L.dy_perm,
+                                                             L.g1, L.g2, L.dx_perm, grads, L.ws)) if block else
+             (lambda: abi.dmoe_expert_ffn_bwd_sgd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
                                                              L.dy_perm, W1, b1, W2, b2, 1e-4, L.dh, L.dx_perm,
                                                              L.ws)) if args.sgd else
              (lambda: abi.dmoe_expert_ffn_bwd_recompute(Dm, L.offsets, L.counts, L.x_perm, W1, b1, W2,
@@ -250,6 +293,8 @@ def main():
           ", ".join(f"{n} {v:.3f}" for n, v in ms.items()), file=sys.stderr, flush=True)
 
     alg = algorithmic(wl, counts, args.recompute, args.sgd)
+    if block:
+        alg.update(algorithmic_block(wl, counts))
     peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
     ridge = peak_tf * 1e12 / (PEAK_HBM_GBS * 1e9)
 
@@ -265,8 +310,9 @@ def main():
         return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4)}
 
-    roofline = dict(roof("ffn_fwd"), kernel="grouped_gemm2 (dmoe_expert_ffn_fwd: up- and down-projection "
-                    "launches + 1-block tile plan)", traffic=measured_traffic(wl.name),
+    kern = ("grouped_gemm2 x3 + ln_act_fwd_kernel x2 (dmoe_expert_ffblock_fwd)" if block else
+            "grouped_gemm2 (dmoe_expert_ffn_fwd: up- and down-projection launches + 1-block tile plan)")
+    roofline = dict(roof("ffn_fwd"), kernel=kern, traffic=measured_traffic(wl.name),
                     per_launch={"flops": alg["ffn_fwd"]["flops"], "bytes": alg["ffn_fwd"]["bytes"],
                                 "ms": round(ms["ffn_fwd"], 4)})
     result = {
@@ -287,7 +333,9 @@ def main():
                    "act": wl.act, "p_alive": wl.p_alive, "pass": "fwd+bwd" if wl.backward else "fwd",
                    "activations": "recomputed in backward" if args.recompute else "stored",
                    "expert_update": "fused SGD in the backward" if args.sgd else "gradients returned",
-                   "topk": "among alive experts" if args.alive_topk else "all experts, dead ones weighted 0"},
+                   "topk": "among alive experts" if args.alive_topk else "all experts, dead ones weighted 0",
+                   "expert": ("Linear-LayerNorm-act-Linear-LayerNorm-act-Linear" if block else
+                              "Linear-act-Linear")},
         "roofline": roofline,
         "roofline_ffn_bwd": roof("ffn_bwd") if wl.backward else None,
         "gate_topk": roof("gate_topk"),

@@ -1,4 +1,6 @@
-"""GPU parity at the full workload sizes, in the launch configuration bench.py times.
+"""GPU parity at the full workload sizes, in the launch configuration bench.py times
+(the four large Linear-act-Linear workloads, and the LayerNorm block workload in
+test_fullsize_ffblock).
 
 Inputs are drawn on the GPU (the weights of the large workloads do not fit the
 host) and the oracle reads back what it needs.  Checked against the oracle:
@@ -178,4 +180,121 @@ def test_fullsize_parity(name):
     del L, W1, b1, W2, b2, x, dy
     if wl.backward:
         del dW1, db1, dW2, db2, dWg, dbg
+    _free()
+
+
+def test_fullsize_ffblock():
+    """The LayerNorm feed-forward block workload at full size (131072 tokens, d_model
+    1024, blocks 1024 -> 4096 -> 4096 -> 1024, 16x16 grid, top-4), in the launch
+    configuration bench.py times.  The LayerNorm scale and shift use the "split"
+    initialisation (scale 1/2, shift +-3 per feature) so that no ReLU decision lies
+    near its kink (asserted) and the backward compares element by element; the
+    kernels and launch shapes do not depend on these values.  Checked: routing and
+    dispatch of every token; every kept tensor, row gradient and parameter gradient
+    of two sampled experts (the busiest and a median one); y, dw, dg and dx of sampled
+    tokens through single-row evaluations of their experts."""
+    import dataclasses
+    from paper_2002_04013_amd import DMoEBlockLayer
+    from workloads import BLOCK_PARAMS, make_block_experts
+    wl = dataclasses.replace(get_workload("ffblock"), ln_init="split")
+    say(f"[fullsize] ffblock: T={wl.T} D={wl.D} F={wl.H} grid {wl.M}^{wl.d} k={wl.k} ln_init={wl.ln_init}")
+    dev = torch.device("cuda")
+    store = O.round_bf16
+    rtol = RTOL[wl.dtype]
+    Wg, bg = make_gate(wl, dev)
+    x, dy, alive = make_x(wl, dev), make_dy(wl, dev), make_alive(wl, dev)
+    prm = make_block_experts(wl, dev)
+    L = DMoEBlockLayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev)
+    L.forward(x, Wg, bg, alive, prm)
+    grads = {n: torch.full_like(v, 7.0) for n, v in prm.items()}
+    dWg, dbg = torch.empty_like(Wg), torch.empty_like(bg)
+    L.backward(dy, x, Wg, alive, prm, grads, dWg, dbg)
+    torch.cuda.synchronize()
+    say("[fullsize] ffblock: GPU pass done")
+
+    x64, Wg64, bg64, dy64 = O.to64(x), O.to64(Wg), O.to64(bg), O.to64(dy)
+    alive_h = alive.cpu().numpy()
+    S = O.gate_scores(x64, Wg64, bg64)
+    idx, _ = O.topk_bruteforce(O.decision_scores(S), wl.d, wl.M, wl.k)
+    g = O.chosen_totals(S, idx, wl.d, wl.M)
+    w = O.mixture_weights(g, idx, alive_h)
+    check_gate(wl, L.scores, L.w, None, S, w, g, x64, Wg64)
+    np.testing.assert_array_equal(L.idx.cpu().numpy(), idx, "idx")
+    counts, offsets, row_token, pos = O.dispatch(idx, alive_h, wl.N)
+    np.testing.assert_array_equal(L.counts.cpu().numpy(), counts, "counts")
+    np.testing.assert_array_equal(L.offsets.cpu().numpy(), offsets, "offsets")
+    rows_used = int(offsets[-1])
+    np.testing.assert_array_equal(L.row_token[:rows_used].cpu().numpy(), row_token, "row_token")
+    np.testing.assert_array_equal(L.pos.cpu().numpy(), pos, "pos")
+    live = np.nonzero(counts)[0]
+    say(f"[fullsize] ffblock: routing + dispatch exact; {rows_used} rows, max rows/expert {counts.max()}")
+
+    row_pair = np.empty(rows_used, np.int64)
+    ok = pos >= 0
+    row_pair[pos[ok]] = np.nonzero(ok.reshape(-1))[0]
+    cache = {}
+
+    def expert(e):
+        if e not in cache:
+            cache[e] = {n: O.to64(prm[n][e]) for n in BLOCK_PARAMS}
+        return cache[e]
+
+    by_count = live[np.argsort(-counts[live], kind="stable")]
+    sample_e = sorted({int(by_count[0]), int(by_count[len(by_count) // 2])})
+    for e in sample_e:
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        p = expert(e)
+        X = x64[row_token[lo:hi]]
+        fw = O.ffblock_forward_stored(X, p, wl.act, store)
+        for hn, gn, bn in (("h1", "g1", "be1"), ("h2", "g2", "be2")):
+            z = O.layernorm_act_forward(fw[hn], p[gn], p[bn], wl.act)["z"]
+            assert np.abs(z).min() > 1e-2, (e, hn, np.abs(z).min())
+        for n in ("h1", "a1", "h2", "a2"):
+            assert_close(L.acts[n][lo:hi], fw[n], rtol, f"{n}[e={e}]")
+        assert_close(L.y_perm[lo:hi], fw["y"], rtol, f"y_perm[e={e}]")
+        pr = row_pair[lo:hi]
+        dY = store(w.reshape(-1)[pr][:, None] * dy64[pr // wl.k])
+        bw = O.ffblock_backward(X, fw, dY, p, wl.act, store)
+        assert_close(L.dy_perm[lo:hi], dY, rtol, f"dy_perm[e={e}]")
+        assert_close(L.g2[lo:hi], bw["dh2"], rtol, f"dh2[e={e}]")
+        assert_close(L.g1[lo:hi], bw["dh1"], rtol, f"dh1[e={e}]")
+        assert_close(L.dx_perm[lo:hi], bw["dX"], rtol, f"dx_perm[e={e}]")
+        for n in BLOCK_PARAMS:
+            assert_close(grads[n][e], bw["grads"][n], rtol, f"d{n}[{e}]")
+        say(f"[fullsize] ffblock: expert {e} ({hi - lo} rows) ok")
+    for e in np.nonzero(counts == 0)[0][:3]:
+        assert bool((grads["W1"][int(e)][:4].float() == 7.0).all()), f"dW1[{e}] written"
+
+    rng = np.random.default_rng(1)
+    toks = sorted(int(t) for t in rng.choice(wl.T, size=4, replace=False))
+    y_ref, dw_ref, dg_ref, dx_ref = [], [], [], []
+    for t in toks:
+        yt, dwt, outs = np.zeros(wl.D), np.zeros(wl.k), []
+        for j in range(wl.k):
+            e = int(idx[t, j])
+            if not alive_h[e]:
+                outs.append(None)
+                continue
+            fw = O.ffblock_forward_stored(x64[t:t + 1], expert(e), wl.act, store)
+            yt += w[t, j] * fw["y"][0]
+            dwt[j] = float(dy64[t] @ fw["y"][0])
+            outs.append(fw)
+        dgt, _, dx_gate, _, _ = O.gate_backward(w[t:t + 1], dwt[None, :], idx[t:t + 1], alive_h, x64[t:t + 1],
+                                               Wg64, wl.d, wl.M)
+        dxt = dx_gate[0].copy()
+        for j, fw in enumerate(outs):
+            if fw is not None:
+                dY = store(w[t, j] * dy64[t:t + 1])
+                dxt += O.ffblock_backward(x64[t:t + 1], fw, dY, expert(int(idx[t, j])), wl.act, store)["dX"][0]
+        y_ref.append(yt)
+        dw_ref.append(dwt)
+        dg_ref.append(dgt[0])
+        dx_ref.append(dxt)
+    tsel = torch.tensor(toks, device=dev)
+    assert_close(L.y[tsel], np.array(y_ref), rtol, "y (sampled tokens)")
+    assert_close(L.dw[tsel], np.array(dw_ref), rtol, "dw (sampled tokens)")
+    assert_close(L.dg[tsel], np.array(dg_ref), rtol, "dg (sampled tokens)")
+    assert_close(L.dx[tsel], np.array(dx_ref), rtol, "dx (sampled tokens)")
+    say(f"[fullsize] ffblock: sampled tokens {toks} ok")
+    del L, prm, grads, x, dy
     _free()
