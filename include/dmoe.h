@@ -29,7 +29,7 @@
  *     offsets[N], stays on the device (no host synchronisation on the path).
  *   - Results are bitwise reproducible from run to run (no floating-point atomics).
  *   - Supported: 1 <= d <= 4, 1 <= M, d*M <= 128, 1 <= k <= min(N, 8),
- *     N <= 16384, T >= 0, D and H multiples of 64, pointers 16-byte aligned.
+ *     N <= 16384, T >= 0, D and H multiples of 64 and at most 2^22, pointers 16-byte aligned.
  *
  * Return codes: DMOE_OK (0); DMOE_EINVAL (-1) null required pointer or bad
  * dims; DMOE_EUNSUPPORTED (-2) shape/alignment outside the supported set;

@@ -30,6 +30,11 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void g2l_16(const void* g, void* lds_wave_base) {
   __builtin_amdgcn_global_load_lds((glb_ptr_t)g, (lds_ptr_t)lds_wave_base, 16, 0, 0);
 }
+// The same from a wave-uniform base and a 32-bit per-lane byte offset: one address
+// register per load instead of a 64-bit pointer (the scalar-base addressing form).
+__device__ __forceinline__ void g2l_16_at(const bf16* base, uint32_t off_bytes, void* lds_wave_base) {
+  g2l_16(reinterpret_cast<const char*>(base) + off_bytes, lds_wave_base);
+}
 
 // s_waitcnt vmcnt(n) with expcnt/lgkmcnt left free (gfx9 encoding).
 template <int N>
@@ -76,7 +81,7 @@ struct KcTile {
       const int r = q * RPI + lane / CH;
       const int c = (lane % CH) ^ swz_kc<BK, SW>(r);
       const int rr = r < rvalid ? r : rvalid - 1;
-      g2l_16(base + (int64_t)rr * ld + c * 8, lds + q * 1024);
+      g2l_16_at(base, ((uint32_t)rr * (uint32_t)ld + (uint32_t)(c * 8)) * 2u, lds + q * 1024);
     }
   }
   // fragment of rows r0 + (lane % 32), k chunk kc + lane / 32 (8 bf16)
@@ -110,7 +115,7 @@ struct NcTile {
       int col = c * 8;
       col = col < cvalid ? col : ((cvalid - 1) & ~7);
       const int kk = k < kvalid ? k : kvalid - 1;
-      g2l_16(base + (int64_t)kk * ld + col, lds + q * 1024);
+      g2l_16_at(base, ((uint32_t)kk * (uint32_t)ld + (uint32_t)col) * 2u, lds + q * 1024);
     }
   }
   // zero rows [kvalid, BK) of the tile (GROUP_K tail)
