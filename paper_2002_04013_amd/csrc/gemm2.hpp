@@ -187,7 +187,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
   constexpr int ABYTES = TA::BYTES, SBYTES = TA::BYTES + TB::BYTES;
   constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave
   // store instructions of a full tile's epilogue, per wave
-  constexpr int SFULL = TM * TN * 4 * (EPI == EPI_BIAS_ACT ? 2 : 1);
+  constexpr int SFULL = EPI == EPI_F32 ? TM * TN * 4 : TM * TN * 2 * (EPI == EPI_BIAS_ACT ? 2 : 1);
   static_assert(TM >= 1 && TM <= 4 && TN >= 1, "tile");
   static_assert(KK % 2 == 0, "fragment slots alternate over an even number of steps");
   static_assert(TA::INSTR % NW == 0 && TB::INSTR % NW == 0, "equal load counts per wave");
@@ -444,10 +444,10 @@ grouped_gemm2(GemmArgs<bf16> p) {
       }
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
+        uint32_t pk[4][2], pa[4][2];      // bf16 pairs of column group g (output, activation)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int nl_ = wn * WTN + i * 32 + 8 * g + 4 * lhi;
-          if (!mok || nl_ >= nvalid) continue;
           const int n = n0 + nl_;
           float v[4];
 #pragma unroll
@@ -472,16 +472,45 @@ grouped_gemm2(GemmArgs<bf16> p) {
             v[3] = __uint_as_float(wv.y & 0xffff0000u) - p.lr * v[3];
           }
           if constexpr (EPI == EPI_F32) {
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) = make_float4(v[0], v[1], v[2], v[3]);
+            if (mok && nl_ < nvalid)
+              *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) = make_float4(v[0], v[1], v[2], v[3]);
           } else {
-            bf16* cp = reinterpret_cast<bf16*>(p.C) + crow + n;
-            *reinterpret_cast<uint2*>(cp) = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
+            pk[g][0] = f2bf2(v[0], v[1]);
+            pk[g][1] = f2bf2(v[2], v[3]);
             if constexpr (EPI == EPI_BIAS_ACT) {
               float a[4];
 #pragma unroll
               for (int r = 0; r < 4; ++r) a[r] = act_fwd_fast(v[r], p.act);
-              bf16* ap = reinterpret_cast<bf16*>(p.C2) + crow + n;
-              *reinterpret_cast<uint2*>(ap) = make_uint2(f2bf2(a[0], a[1]), f2bf2(a[2], a[3]));
+              pa[g][0] = f2bf2(a[0], a[1]);
+              pa[g][1] = f2bf2(a[2], a[3]);
+            }
+          }
+        }
+        if constexpr (EPI != EPI_F32) {
+          // Lanes l and l + 32 hold the two 4-column halves of each 8-column group of one
+          // row.  Swapping the upper lanes of group 2h with the lower lanes of group 2h+1
+          // leaves lane l with columns 16h .. 16h+7 and lane l + 32 with 16h+8 .. 16h+15,
+          // so each lane writes 16 contiguous bytes (all lanes take part in the swaps).
+#pragma unroll
+          for (int h2 = 0; h2 < 2; ++h2) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+              const auto r = __builtin_amdgcn_permlane32_swap(pk[2 * h2][q], pk[2 * h2 + 1][q], false, false);
+              pk[2 * h2][q] = r[0];
+              pk[2 * h2 + 1][q] = r[1];
+              if constexpr (EPI == EPI_BIAS_ACT) {
+                const auto ra = __builtin_amdgcn_permlane32_swap(pa[2 * h2][q], pa[2 * h2 + 1][q], false, false);
+                pa[2 * h2][q] = ra[0];
+                pa[2 * h2 + 1][q] = ra[1];
+              }
+            }
+            const int c = wn * WTN + i * 32 + 16 * h2 + 8 * lhi;
+            if (mok && c < nvalid) {
+              *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + crow + n0 + c) =
+                  make_uint4(pk[2 * h2][0], pk[2 * h2][1], pk[2 * h2 + 1][0], pk[2 * h2 + 1][1]);
+              if constexpr (EPI == EPI_BIAS_ACT)
+                *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C2) + crow + n0 + c) =
+                    make_uint4(pa[2 * h2][0], pa[2 * h2][1], pa[2 * h2 + 1][0], pa[2 * h2 + 1][1]);
             }
           }
         }
