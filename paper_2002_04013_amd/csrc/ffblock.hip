@@ -28,20 +28,24 @@ __device__ __forceinline__ int row_expert(const int32_t* offsets, int N, int r) 
 
 // fp32 layers use the library's erf; bf16 layers (outputs rounded to 2^-9) the
 // erfc-based forms of common.hpp.
-template <typename E> __device__ __forceinline__ float act_f(float z, int act) {
-  if constexpr (sizeof(E) == 4) return act_fwd(z, act);
-  else return act_fwd_fast(z, act);
+// ACT is the activation (DMOE_RELU or DMOE_GELU), fixed at compile time.
+template <typename E, int ACT> __device__ __forceinline__ float act_f(float z) {
+  if constexpr (sizeof(E) == 4) return act_fwd(z, ACT);
+  else return act_fwd_fast(z, ACT);
 }
-template <typename E> __device__ __forceinline__ float act_b(float z, int act) {
-  if constexpr (sizeof(E) == 4) return act_bwd(z, act);
-  else return act_bwd_fast(z, act);
+template <typename E, int ACT> __device__ __forceinline__ float act_b(float z) {
+  if constexpr (sizeof(E) == 4) return act_bwd(z, ACT);
+  else return act_bwd_fast(z, ACT);
 }
 
 // Contiguous share of the rows [0, offsets[N]) for wave gw of nw.
 struct RowRange { int r0, r1; };
 __device__ __forceinline__ RowRange wave_rows(const int32_t* offsets, int N) {
   const int nw = gridDim.x * (LN_NT / 64);
-  const int gw = blockIdx.x * (LN_NT / 64) + (threadIdx.x >> 6);
+  // the wave index through readfirstlane: every value derived from it is wave-uniform,
+  // so row bounds, the row's expert and its statistics come from scalar loads, whose
+  // waits do not include the wave's outstanding vector loads and stores
+  const int gw = blockIdx.x * (LN_NT / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int P = offsets[N];
   const int per = (P + nw - 1) / nw;
   const int r0 = min(P, gw * per);
@@ -50,9 +54,9 @@ __device__ __forceinline__ RowRange wave_rows(const int32_t* offsets, int N) {
 
 // a = act(g (h - mean) rstd + b) per row, stats[r] = (mean, rstd), g and b of the
 // row's expert.  Lane l holds chunks l, l + 64, ... of the row (16 bytes each).
-template <typename E, int CH>
+template <typename E, int CH, int ACT>
 __global__ void __launch_bounds__(LN_NT)
-ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gamma, const E* beta, int act,
+ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gamma, const E* beta,
                   E* a, float* stats) {
   constexpr int VEC = Vec<E>::N;
   const int lane = threadIdx.x & 63;
@@ -102,7 +106,7 @@ ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gam
       Vec<E>::unpack(*reinterpret_cast<const uint4*>(gr + c * VEC), g);
       Vec<E>::unpack(*reinterpret_cast<const uint4*>(br + c * VEC), b);
 #pragma unroll
-      for (int j = 0; j < VEC; ++j) o[j] = act_f<E>(fmaf(g[j], (x[j] - mean) * rstd, b[j]), act);
+      for (int j = 0; j < VEC; ++j) o[j] = act_f<E, ACT>(fmaf(g[j], (x[j] - mean) * rstd, b[j]));
       *reinterpret_cast<uint4*>(ar + c * VEC) = Vec<E>::pack(o);
     }
     if (lane == 0) *reinterpret_cast<float2*>(stats + 2 * (int64_t)r) = make_float2(mean, rstd);
@@ -113,10 +117,10 @@ ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gam
 //   n = (h - mean) rstd, z = g n + b, dn = da act'(z) g,
 //   dh = rstd (dn - mean_f(dn) - n mean_f(dn n)).
 // The whole row is read before it is written, so dh may alias da.
-template <typename E, int CH>
+template <typename E, int CH, int ACT>
 __global__ void __launch_bounds__(LN_NT)
 ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, int N, int F, const E* gamma,
-                       const E* beta, int act, const E* da, E* dh) {
+                       const E* beta, const E* da, E* dh) {
   constexpr int VEC = Vec<E>::N;
   const int lane = threadIdx.x & 63;
   const RowRange rr = wave_rows(offsets, N);
@@ -154,7 +158,7 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
         const float n = (x[j] - mean) * rstd;
-        const float dn = d[j] * act_b<E>(fmaf(g[j], n, b[j]), act) * g[j];
+        const float dn = d[j] * act_b<E, ACT>(fmaf(g[j], n, b[j])) * g[j];
         s1 += dn;
         s2 += dn * n;
       }
@@ -173,7 +177,7 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
         const float n = (x[j] - mean) * rstd;
-        const float dn = d[j] * act_b<E>(fmaf(g[j], n, b[j]), act) * g[j];
+        const float dn = d[j] * act_b<E, ACT>(fmaf(g[j], n, b[j])) * g[j];
         o[j] = rstd * (dn - m1 - n * m2);
       }
       *reinterpret_cast<uint4*>(out + c * VEC) = Vec<E>::pack(o);
@@ -185,10 +189,10 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
 //   dgamma[e][f] = sum over e's rows of da act'(z) n,  dbeta[e][f] = sum of da act'(z).
 // Block (x, e) takes 256 * VEC features of expert e and walks its rows in order.
 // Experts without rows are left untouched.
-template <typename E>
+template <typename E, int ACT>
 __global__ void __launch_bounds__(256)
 ln_act_bwd_params_kernel(const E* h, const float* stats, const int32_t* offsets, int F, const E* gamma,
-                         const E* beta, int act, const E* da, E* dgamma, E* dbeta) {
+                         const E* beta, const E* da, E* dgamma, E* dbeta) {
   constexpr int VEC = Vec<E>::N;
   const int e = blockIdx.y;
   const int r0 = offsets[e], r1 = offsets[e + 1];
@@ -219,7 +223,7 @@ ln_act_bwd_params_kernel(const E* h, const float* stats, const int32_t* offsets,
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
         const float n = (x[j] - st[u].x) * st[u].y;
-        const float dz = d[j] * act_b<E>(fmaf(g[j], n, b[j]), act);
+        const float dz = d[j] * act_b<E, ACT>(fmaf(g[j], n, b[j]));
         ag[j] += dz * n;
         ab[j] += dz;
       }
@@ -233,7 +237,7 @@ ln_act_bwd_params_kernel(const E* h, const float* stats, const int32_t* offsets,
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
       const float n = (x[j] - st.x) * st.y;
-      const float dz = d[j] * act_b<E>(fmaf(g[j], n, b[j]), act);
+      const float dz = d[j] * act_b<E, ACT>(fmaf(g[j], n, b[j]));
       ag[j] += dz * n;
       ab[j] += dz;
     }
@@ -256,32 +260,44 @@ static int ln_grid(const Shape& s) {
   return (int)((waves + LN_NT / 64 - 1) / (LN_NT / 64));
 }
 
+template <typename E, int ACT>
+static void ln_fwd_act(const Shape& s, const int32_t* offsets, const E* h, const E* g, const E* b, E* a,
+                       float* stats, hipStream_t st) {
+  const int N = (int)s.N, F = (int)s.H, grid = ln_grid(s);
+  switch (ln_chunks<E>(F)) {
+    case 1: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 1, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
+    case 2: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 2, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
+    case 4: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 4, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
+    default: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 8, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
+  }
+}
 template <typename E>
 static void ln_fwd(const Shape& s, const int32_t* offsets, const E* h, const E* g, const E* b, E* a,
                    float* stats, hipStream_t st) {
-  const int N = (int)s.N, F = (int)s.H, grid = ln_grid(s);
-  switch (ln_chunks<E>(F)) {
-    case 1: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 1>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, s.act, a, stats); break;
-    case 2: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 2>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, s.act, a, stats); break;
-    case 4: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 4>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, s.act, a, stats); break;
-    default: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 8>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, s.act, a, stats); break;
-  }
+  if (s.act == DMOE_RELU) ln_fwd_act<E, DMOE_RELU>(s, offsets, h, g, b, a, stats, st);
+  else ln_fwd_act<E, DMOE_GELU>(s, offsets, h, g, b, a, stats, st);
 }
 
 // scale and shift gradients first (they read da), then dh (which may overwrite da)
+template <typename E, int ACT>
+static void ln_bwd_act(const Shape& s, const int32_t* offsets, const E* h, const float* stats, const E* g,
+                       const E* b, const E* da, E* dh, E* dg, E* db, hipStream_t st) {
+  const int N = (int)s.N, F = (int)s.H, grid = ln_grid(s);
+  constexpr int VEC = Vec<E>::N;
+  hipLaunchKernelGGL((ln_act_bwd_params_kernel<E, ACT>), dim3((unsigned)((F / VEC + 255) / 256), (unsigned)N),
+                     dim3(256), 0, st, h, stats, offsets, F, g, b, da, dg, db);
+  switch (ln_chunks<E>(F)) {
+    case 1: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 1, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
+    case 2: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 2, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
+    case 4: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 4, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
+    default: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 8, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
+  }
+}
 template <typename E>
 static void ln_bwd(const Shape& s, const int32_t* offsets, const E* h, const float* stats, const E* g, const E* b,
                    const E* da, E* dh, E* dg, E* db, hipStream_t st) {
-  const int N = (int)s.N, F = (int)s.H, grid = ln_grid(s);
-  constexpr int VEC = Vec<E>::N;
-  hipLaunchKernelGGL(ln_act_bwd_params_kernel<E>, dim3((unsigned)((F / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
-                     st, h, stats, offsets, F, g, b, s.act, da, dg, db);
-  switch (ln_chunks<E>(F)) {
-    case 1: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 1>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, s.act, da, dh); break;
-    case 2: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 2>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, s.act, da, dh); break;
-    case 4: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 4>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, s.act, da, dh); break;
-    default: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 8>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, s.act, da, dh); break;
-  }
+  if (s.act == DMOE_RELU) ln_bwd_act<E, DMOE_RELU>(s, offsets, h, stats, g, b, da, dh, dg, db, st);
+  else ln_bwd_act<E, DMOE_GELU>(s, offsets, h, stats, g, b, da, dh, dg, db, st);
 }
 
 // ---------------------------------------------------------------- linear layers
