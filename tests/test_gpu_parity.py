@@ -16,7 +16,7 @@ CASES = {
     # bf16, skinny experts (few rows each): 32-row GEMM tiles, ragged rows, dead experts
     "bf16_skinny": Workload("bf16_skinny", 10, T=512, D=256, H=512, d=2, M=8, k=4, dtype="bf16",
                             act="gelu", p_alive=0.8),
-    # bf16, fat experts (hundreds of rows each): 128x128 GEMM tiles
+    # bf16, fat experts (hundreds of rows each): the 256x256-tile GEMM configuration
     "bf16_fat": Workload("bf16_fat", 11, T=2048, D=128, H=256, d=2, M=4, k=2, dtype="bf16",
                          act="gelu", p_alive=0.9),
     # 3-D grid, token count off the tile grid, ReLU
@@ -37,6 +37,10 @@ CASES = {
     # bf16 gate with 128 columns: the exact fp64 gate path
     "bf16_gate128": Workload("bf16_gate128", 17, T=200, D=128, H=128, d=2, M=64, k=8, dtype="bf16",
                              act="relu", p_alive=0.95),
+    # near the largest grid: 25x25x25 = 15625 experts (most without rows), k = 8 (the
+    # largest), 75 gate columns (three MFMA column blocks), 10% dead
+    "bf16_maxgrid": Workload("bf16_maxgrid", 18, T=700, D=64, H=64, d=3, M=25, k=8, dtype="bf16",
+                             act="gelu", p_alive=0.9),
 }
 
 
