@@ -76,3 +76,44 @@ def test_no_cpu_fallback_without_device(lib):
     x = torch.zeros(8, 64)
     with pytest.raises(lib.DmoeError):
         lib.dmoe_combine(dims, x, torch.zeros(8, 2, dtype=torch.int32), torch.zeros(8, 2), x)
+
+
+def _fake(addr=1 << 20):
+    """A 16-byte aligned non-null address; the calls below return before any device work."""
+    return ctypes.c_void_p(addr)
+
+
+def test_new_entry_points_validate_on_host(lib):
+    raw = lib.load()
+    F = lambda: ctypes.c_void_p(1 << 20)
+    dims = lib.make_dims(64, 64, 256, 2, 4, 2, "bf16", "relu")
+    # null parameter / activation structs
+    rc = raw.dmoe_expert_ffblock_fwd(ctypes.byref(dims), F(), F(), None, None, F(), F(), None)
+    assert rc == -1
+    prm = lib.FFBlockParams(*[F() for _ in lib.FFBLOCK_PARAMS])
+    acts = lib.FFBlockActs(*[F() for _ in lib.FFBLOCK_ACTS])
+    # a missing gradient pointer in the struct is rejected
+    grads = lib.FFBlockParams(*[F() for _ in lib.FFBLOCK_PARAMS])
+    grads.W2 = None
+    rc = raw.dmoe_expert_ffblock_bwd(ctypes.byref(dims), F(), F(), ctypes.byref(prm), ctypes.byref(acts), F(),
+                                     F(), F(), F(), ctypes.byref(grads), F(), None)
+    assert rc == -1
+    # LayerNorm rows wider than the register-held row (bf16: 4096 values) are unsupported
+    wide = lib.make_dims(64, 64, 8192, 2, 4, 2, "bf16", "relu")
+    rc = raw.dmoe_expert_ffblock_fwd(ctypes.byref(wide), F(), F(), ctypes.byref(prm), ctypes.byref(acts), F(),
+                                     F(), None)
+    assert rc == -2
+    rc = raw.dmoe_ln_act_fwd(ctypes.byref(wide), F(), F(), F(), F(), F(), F(), None)
+    assert rc == -2
+    # misaligned pointer
+    rc = raw.dmoe_ln_act_fwd(ctypes.byref(dims), F(), ctypes.c_void_p((1 << 20) + 2), F(), F(), F(), F(), None)
+    assert rc == -2
+    # NaN step size for the fused SGD backward
+    rc = raw.dmoe_expert_ffn_bwd_sgd(ctypes.byref(dims), *[F() for _ in range(10)], ctypes.c_float(float("nan")),
+                                     F(), F(), F(), None)
+    assert rc == -1
+    # widths past the 32-bit tile addressing limit
+    assert lib.workspace_bytes(lib.make_dims(64, 1 << 23, 256, 2, 4, 2)) == 0
+    assert lib.workspace_bytes(lib.make_dims(64, 64, 1 << 23, 2, 4, 2)) == 0
+    # unknown flag bits
+    assert lib.workspace_bytes(lib.make_dims(64, 64, 256, 2, 4, 2, flags=4)) == 0
