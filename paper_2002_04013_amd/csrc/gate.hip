@@ -452,45 +452,45 @@ __global__ void __launch_bounds__(GM_NT) gate_topk_mfma(GateMfmaArgs ga) {
   }
 }
 
-// Alive-first ranking of cells: alive before dead, then total desc, then flat asc.
-// A top-KMAX list lives in three register arrays; comparisons are branch-free.
-__device__ __forceinline__ bool key_better(int al, double at, int af, int bl, double bt, int bf) {
-  return (al > bl) | ((al == bl) & ((at > bt) | ((at == bt) & (af < bf))));
+// Order-preserving 64-bit image of an fp64 value (larger value, larger key; no NaN).
+__device__ __forceinline__ uint64_t ord64(double v) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
 }
-__device__ __forceinline__ void key_insert(int (&kl)[KMAX], double (&kt)[KMAX], int (&kf)[KMAX], int l, double t,
-                                           int f) {
-#pragma unroll
-  for (int p = 0; p < KMAX; ++p) {
-    const bool sw = key_better(l, t, f, kl[p], kt[p], kf[p]);
-    const int ol = kl[p], of = kf[p];
-    const double ot = kt[p];
-    kl[p] = sw ? l : ol; kt[p] = sw ? t : ot; kf[p] = sw ? f : of;
-    l = sw ? ol : l; t = sw ? ot : t; f = sw ? of : f;
-  }
+// Cell keys (live, total, ~flat) compared lexicographically: alive first (when ranked
+// that way), then the larger total, then the lower flat index (larger ~flat).
+__device__ __forceinline__ bool cell_gt(uint32_t al, uint64_t at, uint32_t an, uint32_t bl, uint64_t bt,
+                                        uint32_t bn) {
+  return (al > bl) | ((al == bl) & ((at > bt) | ((at == bt) & (an > bn))));
 }
 
 // Exact path for the queued tokens: fp64 scores S[c] = sum_k x_k W[c][k] + b[c], then the
 // selection.  One block per token at a time (persistent over the queue); thread
 // (c, slice) sums a contiguous k-slice with four fp64 accumulators over interleaved
 // 8-element groups, and the slices are added in order.
-// ALIVE: TopK among the alive experts: every cell of the grid is ranked by (alive
-// first, total desc, flat asc), the totals adding the d fp32 decision scores in fp64
-// in dimension order; each thread keeps the best k of its cells, and the lists are
-// merged across each wave by shuffles and across the waves by one thread.
+// TopK by its definition: every cell of the grid is ranked by (alive first when ALIVE,
+// total desc, flat asc), the totals adding the d fp32 decision scores in fp64 in
+// dimension order.  The k best are found in k rounds; round r takes the best cell that
+// ranks strictly after the winner of round r-1 (the order is total, so no cell is taken
+// twice): each thread scans its cells, then a wave reduction by shuffles and a
+// reduction over the waves in LDS.  Eq. 1 weights cover the chosen experts that are
+// alive.
 template <typename E, bool ALIVE>
 __global__ void __launch_bounds__(GX_NT) gate_exact_kernel(GateArgs a, const int32_t* queue) {
   __shared__ double s64[DM_MAX];
   __shared__ double part[GX_NT];
-  __shared__ int wl_l[GX_NT / 64][KMAX], wl_f[GX_NT / 64][KMAX];
-  __shared__ double wl_t[GX_NT / 64][KMAX];
+  __shared__ uint32_t red_l[GX_NT / 64], red_n[GX_NT / 64];
+  __shared__ uint64_t red_t[GX_NT / 64];
+  __shared__ int32_t chosen[KMAX];
   const int tid = threadIdx.x;
+  const int lane = tid & 63, wid = tid >> 6;
   const int dM = a.dM;
   const int n = queue[0];
   const E* x = reinterpret_cast<const E*>(a.x);
   const E* W = reinterpret_cast<const E*>(a.Wg);
   const E* bg = reinterpret_cast<const E*>(a.bg);
   constexpr int VEC = 16 / sizeof(E);
-  const int S = GX_NT / dM;                                  // k-slices (dM <= DM_MAX = 128 -> S >= 2)
+  const int S = GX_NT / dM;                                  // k-slices (dM <= DM_MAX = 128 -> S >= 4)
   const int KS = (a.D / (4 * VEC) + S - 1) / S * (4 * VEC);  // k per slice, multiple of 4 vectors
   const int c = tid % dM, sl = tid / dM;
   for (int qi = blockIdx.x; qi < n; qi += gridDim.x) {
@@ -525,80 +525,78 @@ __global__ void __launch_bounds__(GX_NT) gate_exact_kernel(GateArgs a, const int
       s64[tid] = v + (bg ? (double)ldf(bg + tid) : 0.0);
     }
     __syncthreads();
-    if constexpr (!ALIVE) {
-      if (tid == 0)
-        select_token<false>(s64, nullptr, a.alive, a.d, a.M, a.k, a.N, 0.f, a.idx + (int64_t)t * a.k,
-                            a.w + (int64_t)t * a.k, a.g ? a.g + (int64_t)t * a.k : nullptr);
-    } else {
-      int kl[KMAX], kf[KMAX];
-      double kt[KMAX];
-#pragma unroll
-      for (int p = 0; p < KMAX; ++p) { kl[p] = -1; kt[p] = -INFINITY; kf[p] = 0x7fffffff; }
+    // k rounds of "best cell after the previous winner"
+    uint32_t pl = 2, pn = 0xffffffffu;                       // above every real key
+    uint64_t pt = ~0ull;
+#pragma unroll 1
+    for (int r = 0; r < a.k; ++r) {
+      uint32_t bl = 0, bn = 0;                               // below every real key (~flat > 0)
+      uint64_t bt = 0;
       for (int f = tid; f < a.N; f += GX_NT) {
-        int rem = f, u[DMAX];
+        int rem = f;
+        double tot = 0.0;
+        int u[DMAX];
 #pragma unroll
         for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < a.d) { u[i] = rem % a.M; rem /= a.M; } }
-        double tot = 0.0;
 #pragma unroll
         for (int i = 0; i < DMAX; ++i) if (i < a.d) tot += (double)(float)s64[i * a.M + u[i]];
-        const int live = a.alive == nullptr || a.alive[f] != 0 ? 1 : 0;
-        key_insert(kl, kt, kf, live, tot, f);
+        const uint32_t l = !ALIVE || a.alive == nullptr || a.alive[f] != 0 ? 1u : 0u;
+        const uint64_t tk = ord64(tot + 0.0);                // -0 and +0 are one value
+        const uint32_t nk = ~(uint32_t)f;
+        if (cell_gt(pl, pt, pn, l, tk, nk) && cell_gt(l, tk, nk, bl, bt, bn)) { bl = l; bt = tk; bn = nk; }
       }
-      // merge across the wave: lane takes the partner's list at distance 32, 16, .., 1
-#pragma unroll
+#pragma unroll 1
       for (int off = 32; off > 0; off >>= 1) {
-        int ol[KMAX], of[KMAX];
-        double ot[KMAX];
-#pragma unroll
-        for (int p = 0; p < KMAX; ++p) {
-          ol[p] = __shfl_xor(kl[p], off, 64);
-          ot[p] = __shfl_xor(kt[p], off, 64);
-          of[p] = __shfl_xor(kf[p], off, 64);
-        }
-#pragma unroll
-        for (int p = 0; p < KMAX; ++p) key_insert(kl, kt, kf, ol[p], ot[p], of[p]);
+        const uint32_t ol = __shfl_xor(bl, off, 64), on = __shfl_xor(bn, off, 64);
+        const uint32_t olo = __shfl_xor((uint32_t)bt, off, 64), ohi = __shfl_xor((uint32_t)(bt >> 32), off, 64);
+        const uint64_t ot = ((uint64_t)ohi << 32) | olo;
+        if (cell_gt(ol, ot, on, bl, bt, bn)) { bl = ol; bt = ot; bn = on; }
       }
-      if ((tid & 63) == 0) {
-#pragma unroll
-        for (int p = 0; p < KMAX; ++p) { wl_l[tid >> 6][p] = kl[p]; wl_t[tid >> 6][p] = kt[p]; wl_f[tid >> 6][p] = kf[p]; }
-      }
+      if (lane == 0) { red_l[wid] = bl; red_t[wid] = bt; red_n[wid] = bn; }
       __syncthreads();
-      if (tid == 0) {
-        for (int w = 1; w < GX_NT / 64; ++w)
+      bl = red_l[0]; bt = red_t[0]; bn = red_n[0];
+#pragma unroll 1
+      for (int w = 1; w < GX_NT / 64; ++w)
+        if (cell_gt(red_l[w], red_t[w], red_n[w], bl, bt, bn)) { bl = red_l[w]; bt = red_t[w]; bn = red_n[w]; }
+      if (tid == 0) chosen[r] = (int32_t)~bn;
+      pl = bl; pt = bt; pn = bn;
+      __syncthreads();                                       // red_* reused by the next round
+    }
+    if (tid == 0) {
+      // Eq. 1 weights from the fp64 totals of the chosen experts, over the alive ones
+      double gx[KMAX];
+      bool lv[KMAX];
+      double m = -1.0e308;
+      bool any = false;
 #pragma unroll
-          for (int p = 0; p < KMAX; ++p) key_insert(kl, kt, kf, wl_l[w][p], wl_t[w][p], wl_f[w][p]);
-        // Eq. 1 weights from the fp64 totals of the chosen experts, over the alive ones
-        double gx[KMAX];
-        double m = -1.0e308;
-        bool any = false;
+      for (int j = 0; j < KMAX; ++j) {
+        gx[j] = 0.0;
+        lv[j] = false;
+        if (j < a.k) {
+          int rem = chosen[j], u[DMAX];
 #pragma unroll
-        for (int j = 0; j < KMAX; ++j) {
-          gx[j] = 0.0;
-          if (j < a.k) {
-            int rem = kf[j], u[DMAX];
+          for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < a.d) { u[i] = rem % a.M; rem /= a.M; } }
+          double tt = 0.0;
 #pragma unroll
-            for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < a.d) { u[i] = rem % a.M; rem /= a.M; } }
-            double tt = 0.0;
-#pragma unroll
-            for (int i = 0; i < DMAX; ++i) if (i < a.d) tt += s64[i * a.M + u[i]];
-            gx[j] = tt;
-            if (kl[j] > 0) { any = true; m = tt > m ? tt : m; }
-          }
+          for (int i = 0; i < DMAX; ++i) if (i < a.d) tt += s64[i * a.M + u[i]];
+          gx[j] = tt;
+          lv[j] = a.alive == nullptr || a.alive[chosen[j]] != 0;
+          if (lv[j]) { any = true; m = tt > m ? tt : m; }
         }
-        float ex[KMAX];
-        float sum = 0.f;
+      }
+      float ex[KMAX];
+      float sum = 0.f;
 #pragma unroll
-        for (int j = 0; j < KMAX; ++j) {
-          ex[j] = j < a.k && kl[j] > 0 ? expf((float)(gx[j] - m)) : 0.f;
-          sum += ex[j];
-        }
+      for (int j = 0; j < KMAX; ++j) {
+        ex[j] = lv[j] ? expf((float)(gx[j] - m)) : 0.f;
+        sum += ex[j];
+      }
 #pragma unroll
-        for (int j = 0; j < KMAX; ++j) {
-          if (j < a.k) {
-            a.idx[(int64_t)t * a.k + j] = kf[j];
-            a.w[(int64_t)t * a.k + j] = any ? ex[j] / sum : 0.f;
-            if (a.g) a.g[(int64_t)t * a.k + j] = (float)gx[j];
-          }
+      for (int j = 0; j < KMAX; ++j) {
+        if (j < a.k) {
+          a.idx[(int64_t)t * a.k + j] = chosen[j];
+          a.w[(int64_t)t * a.k + j] = any ? ex[j] / sum : 0.f;
+          if (a.g) a.g[(int64_t)t * a.k + j] = (float)gx[j];
         }
       }
     }
