@@ -132,7 +132,7 @@ def cpu_baseline(wl, inp, counts, budget_s=12.0):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_wide.json")
-KERNEL_SOURCES = ("gemm.hpp", "gemm2.hpp", "ffn.hip", "common.hpp")
+KERNEL_SOURCES = ("gemm.hpp", "gemm2.hpp", "grouped.hpp", "ffn.hip", "common.hpp")
 
 
 def kernel_source_hash():

@@ -65,7 +65,22 @@ segment_colsum(const E* X, int64_t ld, const int32_t* offsets, int ncols, E* out
   float acc[VEC];
 #pragma unroll
   for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
-  for (int r = r0; r < r1; ++r) {
+  // rows in order; four loads in flight at a time
+  constexpr int U = 4;
+  int r = r0;
+  for (; r + U <= r1; r += U) {
+    uint4 q[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) q[u] = *reinterpret_cast<const uint4*>(X + (int64_t)(r + u) * ld + c);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float v[VEC];
+      Vec<E>::unpack(q[u], v);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) acc[i] += v[i];
+    }
+  }
+  for (; r < r1; ++r) {
     float v[VEC];
     Vec<E>::unpack(*reinterpret_cast<const uint4*>(X + (int64_t)r * ld + c), v);
 #pragma unroll
