@@ -53,7 +53,10 @@ __device__ __forceinline__ RowRange wave_rows(const int32_t* offsets, int N) {
 }
 
 // a = act(g (h - mean) rstd + b) per row, stats[r] = (mean, rstd), g and b of the
-// row's expert.  Lane l holds chunks l, l + 64, ... of the row (16 bytes each).
+// row's expert.  Lane l holds chunks l, l + 64, ... of the row (16 bytes each).  The
+// next row is loaded before this row's results are stored (vector-memory operations
+// retire in order, so a row's loads then never wait for the previous row's stores),
+// and the expert's g and b stay in registers until the expert changes.
 template <typename E, int CH, int ACT>
 __global__ void __launch_bounds__(LN_NT)
 ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gamma, const E* beta,
@@ -66,15 +69,25 @@ ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gam
   const float invF = 1.f / (float)F;
   int e = row_expert(offsets, N, rr.r0);
   int eend = offsets[e + 1];
-  for (int r = rr.r0; r < rr.r1; ++r) {
-    while (r >= eend) eend = offsets[++e + 1];
-    const E* hr = h + (int64_t)r * F;
-    uint4 hv[CH];
+  int eg = -1;                                   // expert whose g, b are in gv, bv
+  uint4 hv[CH], gv[CH], bv[CH];
+  auto load_row = [&](uint4 (&v)[CH], const E* src) {
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int c = lane + 64 * i;
-      hv[i] = c < nch ? *reinterpret_cast<const uint4*>(hr + c * VEC) : make_uint4(0, 0, 0, 0);
+      v[i] = c < nch ? *reinterpret_cast<const uint4*>(src + c * VEC) : make_uint4(0, 0, 0, 0);
     }
+  };
+  load_row(hv, h + (int64_t)rr.r0 * F);
+  for (int r = rr.r0; r < rr.r1; ++r) {
+    while (r >= eend) eend = offsets[++e + 1];
+    if (e != eg) {
+      load_row(gv, gamma + (int64_t)e * F);
+      load_row(bv, beta + (int64_t)e * F);
+      eg = e;
+    }
+    uint4 hn[CH];
+    if (r + 1 < rr.r1) load_row(hn, h + (int64_t)(r + 1) * F);
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
@@ -94,8 +107,6 @@ ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gam
       for (int j = 0; j < VEC; ++j) q += (x[j] - mean) * (x[j] - mean);
     }
     const float rstd = 1.f / sqrtf(wave_sum(q) * invF + LN_EPS);
-    const E* gr = gamma + (int64_t)e * F;
-    const E* br = beta + (int64_t)e * F;
     E* ar = a + (int64_t)r * F;
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
@@ -103,20 +114,25 @@ ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gam
       if (c >= nch) continue;
       float x[VEC], g[VEC], b[VEC], o[VEC];
       Vec<E>::unpack(hv[i], x);
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(gr + c * VEC), g);
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(br + c * VEC), b);
+      Vec<E>::unpack(gv[i], g);
+      Vec<E>::unpack(bv[i], b);
 #pragma unroll
       for (int j = 0; j < VEC; ++j) o[j] = act_f<E, ACT>(fmaf(g[j], (x[j] - mean) * rstd, b[j]));
       *reinterpret_cast<uint4*>(ar + c * VEC) = Vec<E>::pack(o);
     }
     if (lane == 0) *reinterpret_cast<float2*>(stats + 2 * (int64_t)r) = make_float2(mean, rstd);
+    if (r + 1 < rr.r1) {
+#pragma unroll
+      for (int i = 0; i < CH; ++i) hv[i] = hn[i];
+    }
   }
 }
 
 // Input gradient of the normalisation step, per row:
 //   n = (h - mean) rstd, z = g n + b, dn = da act'(z) g,
 //   dh = rstd (dn - mean_f(dn) - n mean_f(dn n)).
-// The whole row is read before it is written, so dh may alias da.
+// The whole row is read before it is written, so dh may alias da.  As in the forward,
+// the next row is loaded before this row is stored, and g, b stay in registers.
 template <typename E, int CH, int ACT>
 __global__ void __launch_bounds__(LN_NT)
 ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, int N, int F, const E* gamma,
@@ -129,19 +145,28 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
   const float invF = 1.f / (float)F;
   int e = row_expert(offsets, N, rr.r0);
   int eend = offsets[e + 1];
-  for (int r = rr.r0; r < rr.r1; ++r) {
-    while (r >= eend) eend = offsets[++e + 1];
-    const E* hr = h + (int64_t)r * F;
-    const E* dr = da + (int64_t)r * F;
-    const E* gr = gamma + (int64_t)e * F;
-    const E* br = beta + (int64_t)e * F;
-    uint4 hv[CH], dv[CH];
+  int eg = -1;
+  uint4 hv[CH], dv[CH], gv[CH], bv[CH];
+  auto load_row = [&](uint4 (&v)[CH], const E* src) {
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int c = lane + 64 * i;
-      const bool ok = c < nch;
-      hv[i] = ok ? *reinterpret_cast<const uint4*>(hr + c * VEC) : make_uint4(0, 0, 0, 0);
-      dv[i] = ok ? *reinterpret_cast<const uint4*>(dr + c * VEC) : make_uint4(0, 0, 0, 0);
+      v[i] = c < nch ? *reinterpret_cast<const uint4*>(src + c * VEC) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  load_row(hv, h + (int64_t)rr.r0 * F);
+  load_row(dv, da + (int64_t)rr.r0 * F);
+  for (int r = rr.r0; r < rr.r1; ++r) {
+    while (r >= eend) eend = offsets[++e + 1];
+    if (e != eg) {
+      load_row(gv, gamma + (int64_t)e * F);
+      load_row(bv, beta + (int64_t)e * F);
+      eg = e;
+    }
+    uint4 hn[CH], dn_[CH];
+    if (r + 1 < rr.r1) {
+      load_row(hn, h + (int64_t)(r + 1) * F);
+      load_row(dn_, da + (int64_t)(r + 1) * F);
     }
     const float2 st = *reinterpret_cast<const float2*>(stats + 2 * (int64_t)r);
     const float mean = st.x, rstd = st.y;
@@ -153,8 +178,8 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
       float x[VEC], d[VEC], g[VEC], b[VEC];
       Vec<E>::unpack(hv[i], x);
       Vec<E>::unpack(dv[i], d);
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(gr + c * VEC), g);
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(br + c * VEC), b);
+      Vec<E>::unpack(gv[i], g);
+      Vec<E>::unpack(bv[i], b);
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
         const float n = (x[j] - mean) * rstd;
@@ -172,8 +197,8 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
       float x[VEC], d[VEC], g[VEC], b[VEC], o[VEC];
       Vec<E>::unpack(hv[i], x);
       Vec<E>::unpack(dv[i], d);
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(gr + c * VEC), g);
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(br + c * VEC), b);
+      Vec<E>::unpack(gv[i], g);
+      Vec<E>::unpack(bv[i], b);
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
         const float n = (x[j] - mean) * rstd;
@@ -181,6 +206,10 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
         o[j] = rstd * (dn - m1 - n * m2);
       }
       *reinterpret_cast<uint4*>(out + c * VEC) = Vec<E>::pack(o);
+    }
+    if (r + 1 < rr.r1) {
+#pragma unroll
+      for (int i = 0; i < CH; ++i) { hv[i] = hn[i]; dv[i] = dn_[i]; }
     }
   }
 }

@@ -465,144 +465,308 @@ __device__ __forceinline__ bool cell_gt(uint32_t al, uint64_t at, uint32_t an, u
 }
 
 // Exact path for the queued tokens: fp64 scores S[c] = sum_k x_k W[c][k] + b[c], then the
-// selection.  One block per token at a time (persistent over the queue); thread
-// (c, slice) sums a contiguous k-slice with four fp64 accumulators over interleaved
-// 8-element groups, and the slices are added in order.
-// TopK by its definition: every cell of the grid is ranked by (alive first when ALIVE,
-// total desc, flat asc), the totals adding the d fp32 decision scores in fp64 in
-// dimension order.  The k best are found in k rounds; round r takes the best cell that
-// ranks strictly after the winner of round r-1 (the order is total, so no cell is taken
-// twice): each thread scans its cells, then a wave reduction by shuffles and a
-// reduction over the waves in LDS.  Eq. 1 weights cover the chosen experts that are
-// alive.
-template <typename E, bool ALIVE>
-__global__ void __launch_bounds__(GX_NT) gate_exact_kernel(GateArgs a, const int32_t* queue) {
-  __shared__ double s64[DM_MAX];
-  __shared__ double part[GX_NT];
-  __shared__ uint32_t red_l[GX_NT / 64], red_n[GX_NT / 64];
-  __shared__ uint64_t red_t[GX_NT / 64];
-  __shared__ int32_t chosen[KMAX];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wid = tid >> 6;
-  const int dM = a.dM;
-  const int n = queue[0];
+// selection.  Persistent blocks over the queue; a pass takes TB tokens: GX_TB = 8 where
+// every token is queued (alive-first TopK, or exact scores asked for: the tokens of a
+// pass share each load of Wg, and one wave selects for each), 1 for the few tokens the
+// certificate rejects (lowest latency, two blocks per compute unit).  Wave w owns the gate columns
+// [w cpw, (w+1) cpw), cpw = ceil(dM / 8), GX_CT at a time; lane l sums the 16-byte
+// vectors l, l + 64, ... of the rows (each wave load is 1 KB of one row) with fp64
+// FMAs of the exact element values, P vectors' loads issued before any is used; a
+// shuffle tree adds the 64 lane sums.
+constexpr int GX_CT = 4;          // gate columns per wave pass of the exact scores
+constexpr int GX_TB = 8;          // tokens per pass when every token is queued (one per wave)
+
+// Element q (compile-time after unrolling) of a 16-byte vector, as a float.
+template <typename E> __device__ __forceinline__ float vec_elem(const uint4& v, int q);
+template <> __device__ __forceinline__ float vec_elem<float>(const uint4& v, int q) {
+  return __uint_as_float(q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w);
+}
+template <> __device__ __forceinline__ float vec_elem<bf16>(const uint4& v, int q) {
+  const uint32_t w = (q >> 1) == 0 ? v.x : (q >> 1) == 1 ? v.y : (q >> 1) == 2 ? v.z : v.w;
+  return __uint_as_float((q & 1) ? (w & 0xffff0000u) : (w << 16));
+}
+
+template <typename E, int TB, int P>
+__device__ __forceinline__ void exact_scores(const GateArgs& a, const int* tok, double (*s64)[DM_MAX]) {
+  constexpr int VEC = 16 / sizeof(E);
+  constexpr int NW = GX_NT / 64;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int cpw = (a.dM + NW - 1) / NW;
+  const int cend = min(a.dM, (w + 1) * cpw);
+  const int nv = a.D / VEC;
   const E* x = reinterpret_cast<const E*>(a.x);
   const E* W = reinterpret_cast<const E*>(a.Wg);
   const E* bg = reinterpret_cast<const E*>(a.bg);
-  constexpr int VEC = 16 / sizeof(E);
-  const int S = GX_NT / dM;                                  // k-slices (dM <= DM_MAX = 128 -> S >= 4)
-  const int KS = (a.D / (4 * VEC) + S - 1) / S * (4 * VEC);  // k per slice, multiple of 4 vectors
-  const int c = tid % dM, sl = tid / dM;
-  for (int qi = blockIdx.x; qi < n; qi += gridDim.x) {
-    const int t = queue[GQ_HEAD + qi];
-    double acc4[4] = {0.0, 0.0, 0.0, 0.0};
-    if (sl < S) {
-      const E* xr = x + (int64_t)t * a.D;
-      const E* wr = W + (int64_t)c * a.D;
-      const int k1 = min(a.D, (sl + 1) * KS);
-      for (int kk = sl * KS; kk < k1; kk += 4 * VEC) {
-        uint4 xv[4], wv[4];
+  for (int c0 = w * cpw; c0 < cend; c0 += GX_CT) {
+    const E* wr[GX_CT];
+    const E* xr[TB];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          xv[u] = *reinterpret_cast<const uint4*>(xr + kk + VEC * u);
-          wv[u] = *reinterpret_cast<const uint4*>(wr + kk + VEC * u);
-        }
+    for (int c = 0; c < GX_CT; ++c) wr[c] = W + (int64_t)min(c0 + c, a.dM - 1) * a.D;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          float xf[VEC], wf[VEC];
-          Vec<E>::unpack(xv[u], xf);
-          Vec<E>::unpack(wv[u], wf);
+    for (int t = 0; t < TB; ++t) xr[t] = x + (int64_t)tok[t] * a.D;
+    double acc[TB][GX_CT];
 #pragma unroll
-          for (int q = 0; q < VEC; ++q) acc4[u] = fma((double)xf[q], (double)wf[q], acc4[u]);
+    for (int t = 0; t < TB; ++t)
+#pragma unroll
+      for (int c = 0; c < GX_CT; ++c) acc[t][c] = 0.0;
+    for (int v0 = lane; v0 < nv; v0 += 64 * P) {
+      uint4 wv[P][GX_CT], xv[P][TB];
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        const int64_t v = v0 + 64 * p;
+        if (v < nv) {
+#pragma unroll
+          for (int c = 0; c < GX_CT; ++c) wv[p][c] = *reinterpret_cast<const uint4*>(wr[c] + v * VEC);
+#pragma unroll
+          for (int t = 0; t < TB; ++t) xv[p][t] = *reinterpret_cast<const uint4*>(xr[t] + v * VEC);
         }
       }
-    }
-    part[tid] = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
-    __syncthreads();
-    if (tid < dM) {
-      double v = 0.0;
-      for (int q = 0; q < S; ++q) v += part[q * dM + tid];
-      s64[tid] = v + (bg ? (double)ldf(bg + tid) : 0.0);
-    }
-    __syncthreads();
-    // k rounds of "best cell after the previous winner"
-    uint32_t pl = 2, pn = 0xffffffffu;                       // above every real key
-    uint64_t pt = ~0ull;
-#pragma unroll 1
-    for (int r = 0; r < a.k; ++r) {
-      uint32_t bl = 0, bn = 0;                               // below every real key (~flat > 0)
-      uint64_t bt = 0;
-      for (int f = tid; f < a.N; f += GX_NT) {
-        int rem = f;
-        double tot = 0.0;
-        int u[DMAX];
 #pragma unroll
-        for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < a.d) { u[i] = rem % a.M; rem /= a.M; } }
+      for (int p = 0; p < P; ++p) {
+        if (v0 + 64 * p < nv) {
 #pragma unroll
-        for (int i = 0; i < DMAX; ++i) if (i < a.d) tot += (double)(float)s64[i * a.M + u[i]];
-        const uint32_t l = !ALIVE || a.alive == nullptr || a.alive[f] != 0 ? 1u : 0u;
-        const uint64_t tk = ord64(tot + 0.0);                // -0 and +0 are one value
-        const uint32_t nk = ~(uint32_t)f;
-        if (cell_gt(pl, pt, pn, l, tk, nk) && cell_gt(l, tk, nk, bl, bt, bn)) { bl = l; bt = tk; bn = nk; }
-      }
-#pragma unroll 1
-      for (int off = 32; off > 0; off >>= 1) {
-        const uint32_t ol = __shfl_xor(bl, off, 64), on = __shfl_xor(bn, off, 64);
-        const uint32_t olo = __shfl_xor((uint32_t)bt, off, 64), ohi = __shfl_xor((uint32_t)(bt >> 32), off, 64);
-        const uint64_t ot = ((uint64_t)ohi << 32) | olo;
-        if (cell_gt(ol, ot, on, bl, bt, bn)) { bl = ol; bt = ot; bn = on; }
-      }
-      if (lane == 0) { red_l[wid] = bl; red_t[wid] = bt; red_n[wid] = bn; }
-      __syncthreads();
-      bl = red_l[0]; bt = red_t[0]; bn = red_n[0];
-#pragma unroll 1
-      for (int w = 1; w < GX_NT / 64; ++w)
-        if (cell_gt(red_l[w], red_t[w], red_n[w], bl, bt, bn)) { bl = red_l[w]; bt = red_t[w]; bn = red_n[w]; }
-      if (tid == 0) chosen[r] = (int32_t)~bn;
-      pl = bl; pt = bt; pn = bn;
-      __syncthreads();                                       // red_* reused by the next round
-    }
-    if (tid == 0) {
-      // Eq. 1 weights from the fp64 totals of the chosen experts, over the alive ones
-      double gx[KMAX];
-      bool lv[KMAX];
-      double m = -1.0e308;
-      bool any = false;
+          for (int q = 0; q < VEC; ++q) {
+            double xd[TB], wd[GX_CT];
 #pragma unroll
-      for (int j = 0; j < KMAX; ++j) {
-        gx[j] = 0.0;
-        lv[j] = false;
-        if (j < a.k) {
-          int rem = chosen[j], u[DMAX];
+            for (int t = 0; t < TB; ++t) xd[t] = (double)vec_elem<E>(xv[p][t], q);
 #pragma unroll
-          for (int i = DMAX - 1; i >= 0; --i) { u[i] = 0; if (i < a.d) { u[i] = rem % a.M; rem /= a.M; } }
-          double tt = 0.0;
+            for (int c = 0; c < GX_CT; ++c) wd[c] = (double)vec_elem<E>(wv[p][c], q);
 #pragma unroll
-          for (int i = 0; i < DMAX; ++i) if (i < a.d) tt += s64[i * a.M + u[i]];
-          gx[j] = tt;
-          lv[j] = a.alive == nullptr || a.alive[chosen[j]] != 0;
-          if (lv[j]) { any = true; m = tt > m ? tt : m; }
-        }
-      }
-      float ex[KMAX];
-      float sum = 0.f;
+            for (int t = 0; t < TB; ++t)
 #pragma unroll
-      for (int j = 0; j < KMAX; ++j) {
-        ex[j] = lv[j] ? expf((float)(gx[j] - m)) : 0.f;
-        sum += ex[j];
-      }
-#pragma unroll
-      for (int j = 0; j < KMAX; ++j) {
-        if (j < a.k) {
-          a.idx[(int64_t)t * a.k + j] = chosen[j];
-          a.w[(int64_t)t * a.k + j] = any ? ex[j] / sum : 0.f;
-          if (a.g) a.g[(int64_t)t * a.k + j] = (float)gx[j];
+              for (int c = 0; c < GX_CT; ++c) acc[t][c] = fma(xd[t], wd[c], acc[t][c]);
+          }
         }
       }
     }
-    if (a.scores && tid < dM) a.scores[(int64_t)t * dM + tid] = (float)s64[tid];
+#pragma unroll
+    for (int t = 0; t < TB; ++t) {
+#pragma unroll
+      for (int c = 0; c < GX_CT; ++c) {
+        double v = acc[t][c];
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        if (lane == 0 && c0 + c < cend) s64[t][c0 + c] = v + (bg ? (double)ldf(bg + c0 + c) : 0.0);
+      }
+    }
+  }
+}
+
+// Cell key (live, ord64(total), ~flat): the lexicographic maximum is the best cell.
+struct CellKey { uint32_t l; uint64_t t; uint32_t n; };
+
+__device__ __forceinline__ bool key_gt(const CellKey& a, const CellKey& b) {
+  return cell_gt(a.l, a.t, a.n, b.l, b.t, b.n);
+}
+__device__ __forceinline__ CellKey key_sel(bool c, const CellKey& a, const CellKey& b) {
+  return CellKey{c ? a.l : b.l, c ? a.t : b.t, c ? a.n : b.n};
+}
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t u64_max_dpp(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)v, (int)(uint32_t)v, CTRL, ROWS, 0xf, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(v >> 32), (int)(uint32_t)(v >> 32), CTRL,
+                                                            ROWS, 0xf, false);
+  const uint64_t o = ((uint64_t)hi << 32) | lo;
+  return o > v ? o : v;
+}
+
+// Maximum of a 64-bit value over the wave (every lane gets it): within each row of 16
+// lanes by DPP exchanges (lane i with i^1, i^2, 7-i, 15-i), then row r-1's last lane into
+// row r (rows 1 and 3) and lane 31 into rows 2 and 3, so that lane 63 holds the maximum.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+  v = u64_max_dpp<0xB1, 0xf>(v);       // quad_perm [1,0,3,2]
+  v = u64_max_dpp<0x4E, 0xf>(v);       // quad_perm [2,3,0,1]
+  v = u64_max_dpp<0x141, 0xf>(v);      // row_half_mirror
+  v = u64_max_dpp<0x140, 0xf>(v);      // row_mirror
+  v = u64_max_dpp<0x142, 0xa>(v);      // row_bcast:15
+  v = u64_max_dpp<0x143, 0xc>(v);      // row_bcast:31
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+}
+
+// TopK by its definition for one token, by one wave: every cell of the grid is ranked by
+// (alive first when ALIVE, total desc, flat asc), the totals adding the d fp32 decision
+// scores sd (as fp64) in fp64 in dimension order.  Lane l scans the cells l, l + 64, ...
+// (mixed-radix digits advanced by 64 per cell, four cells per step) into its own sorted
+// list of the LK >= k best, then k rounds take the best list head of the wave: the
+// largest live flag, then the largest total among those heads, ties to the larger
+// ~flat; the owner drops it.  Eq. 1 weights over the chosen experts that are alive;
+// lane j writes entry j.
+template <bool ALIVE, int LK>
+__device__ __forceinline__ void exact_select_wave(const GateArgs& a, const double* sc, const double* sd,
+                                                  const uint8_t* alv, int t) {
+  const int lane = threadIdx.x & 63;
+  const int d = a.d, M = a.M, k = a.k, N = a.N;
+  const CellKey none{0u, 0ull, 0u};                                 // below every real key
+  CellKey L[LK];
+#pragma unroll
+  for (int j = 0; j < LK; ++j) L[j] = none;
+  int u[DMAX], st[DMAX];
+  {
+    int rl = lane, rs = 64;
+#pragma unroll
+    for (int i = DMAX - 1; i >= 0; --i) {
+      u[i] = 0; st[i] = 0;
+      if (i < d) { u[i] = rl % M; rl /= M; st[i] = rs % M; rs /= M; }
+    }
+  }
+  for (int f0 = lane; f0 < N; f0 += 4 * 64) {
+    CellKey c[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int f = f0 + 64 * q;
+      double tot = 0.0;
+#pragma unroll
+      for (int i = 0; i < DMAX; ++i) if (i < d) tot += sd[i * M + u[i]];   // digits stay in [0, M)
+      const uint32_t live = !ALIVE || alv[min(f, N - 1)] != 0 ? 1u : 0u;
+      c[q] = key_sel(f < N, CellKey{live, ord64(tot + 0.0), ~(uint32_t)f}, none);   // -0 and +0 are one value
+      int carry = 0;                                                  // digits of f + 64
+#pragma unroll
+      for (int i = DMAX - 1; i >= 0; --i) {
+        if (i < d) {
+          u[i] += st[i] + carry;
+          carry = u[i] >= M;
+          u[i] -= carry ? M : 0;
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {                                     // sorted insertion, no branches
+      CellKey cur = c[q];
+      bool go = false;
+#pragma unroll
+      for (int j = 0; j < LK; ++j) {
+        const bool gt = go || key_gt(cur, L[j]);
+        const CellKey old = L[j];
+        L[j] = key_sel(gt, cur, old);
+        cur = key_sel(gt, old, cur);
+        go = gt;
+      }
+    }
+  }
+  int chosen[KMAX];
+#pragma unroll
+  for (int r = 0; r < KMAX; ++r) {
+    chosen[r] = 0;
+    if (r < k) {
+      const CellKey h = L[0];
+      uint32_t lmax = 1u;
+      if (ALIVE) lmax = __ballot(h.l != 0u) != 0ull ? 1u : 0u;
+      const uint64_t tt = h.l == lmax ? h.t : 0ull;                  // real totals have keys > 0
+      const uint64_t tmax = wave_max_u64(tt);
+      const uint64_t mask = __ballot(tt == tmax && h.l == lmax);
+      int wl;
+      if (__popcll(mask) == 1) {
+        wl = __ffsll((unsigned long long)mask) - 1;
+      } else {                                                       // equal totals: larger ~flat
+        const uint64_t nn = (mask >> lane) & 1ull ? (uint64_t)h.n : 0ull;
+        const uint64_t nmax = wave_max_u64(nn);
+        wl = __ffsll((unsigned long long)__ballot(nn == nmax && ((mask >> lane) & 1ull))) - 1;
+      }
+      wl = __builtin_amdgcn_readfirstlane(wl);
+      chosen[r] = (int)~(uint32_t)__builtin_amdgcn_readlane((int)h.n, wl);
+      const bool pop = lane == wl;
+#pragma unroll
+      for (int j = 0; j < LK - 1; ++j) L[j] = key_sel(pop, L[j + 1], L[j]);
+      L[LK - 1] = key_sel(pop, none, L[LK - 1]);
+    }
+  }
+  // Eq. 1 weights from the fp64 totals of the chosen experts, over the alive ones
+  // (uniform over the wave; lane j stores entry j)
+  double gx[KMAX];
+  bool lv[KMAX];
+  double m = -1.0e308;
+  bool any = false;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    gx[j] = 0.0;
+    lv[j] = false;
+    if (j < k) {
+      int rem = chosen[j], v[DMAX];
+#pragma unroll
+      for (int i = DMAX - 1; i >= 0; --i) { v[i] = 0; if (i < d) { v[i] = rem % M; rem /= M; } }
+      double tt = 0.0;
+#pragma unroll
+      for (int i = 0; i < DMAX; ++i) if (i < d) tt += sc[i * M + v[i]];
+      gx[j] = tt;
+      lv[j] = a.alive == nullptr || a.alive[chosen[j]] != 0;
+      if (lv[j]) { any = true; m = tt > m ? tt : m; }
+    }
+  }
+  float ex[KMAX];
+  float sum = 0.f;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    ex[j] = lv[j] ? expf((float)(gx[j] - m)) : 0.f;
+    sum += ex[j];
+  }
+  int my_idx = 0;
+  float my_w = 0.f, my_g = 0.f;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (lane == j) { my_idx = chosen[j]; my_w = any ? ex[j] / sum : 0.f; my_g = (float)gx[j]; }
+  }
+  if (lane < k) {
+    a.idx[(int64_t)t * k + lane] = my_idx;
+    a.w[(int64_t)t * k + lane] = my_w;
+    if (a.g) a.g[(int64_t)t * k + lane] = my_g;
+  }
+  if (a.scores)
+    for (int c = lane; c < a.dM; c += 64) a.scores[(int64_t)t * a.dM + c] = (float)sc[c];
+}
+
+template <typename E, bool ALIVE, int TB, int P>
+__device__ __forceinline__ void exact_pass(const GateArgs& a, const int32_t* queue, int n, int qg,
+                                           double (*s64)[DM_MAX], double (*sd)[DM_MAX], const uint8_t* alv) {
+  const int nt = min(TB, n - qg * TB);
+  int tok[TB];
+#pragma unroll
+  for (int j = 0; j < TB; ++j) tok[j] = queue[GQ_HEAD + qg * TB + min(j, nt - 1)];   // pads repeat a token
+  exact_scores<E, TB, P>(a, tok, s64);
+  __syncthreads();
+  for (int q = threadIdx.x; q < nt * a.dM; q += GX_NT)
+    sd[q / a.dM][q % a.dM] = (double)(float)s64[q / a.dM][q % a.dM];
+  __syncthreads();
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (w < nt) {
+    if (a.k <= 4) exact_select_wave<ALIVE, 4>(a, s64[w], sd[w], alv, tok[w]);
+    else exact_select_wave<ALIVE, KMAX>(a, s64[w], sd[w], alv, tok[w]);
+  }
+  __syncthreads();                                                   // s64, sd reused by the next pass
+}
+
+template <typename E, bool ALIVE, int TB>
+__device__ __forceinline__ void exact_body(const GateArgs& a, const int32_t* queue, double (*s64)[DM_MAX],
+                                           double (*sd)[DM_MAX], uint8_t* alv) {
+  const int n = queue[0];
+  const int ngrp = (n + TB - 1) / TB;
+  if ((int)blockIdx.x >= ngrp) return;
+  if (ALIVE) {
+    for (int f = threadIdx.x; f < a.N; f += GX_NT) alv[f] = a.alive == nullptr || a.alive[f] != 0 ? 1 : 0;
     __syncthreads();
   }
+  for (int qg = blockIdx.x; qg < ngrp; qg += gridDim.x)
+    exact_pass<E, ALIVE, TB, TB == 1 ? 3 : 2>(a, queue, n, qg, s64, sd, alv);
+}
+
+// Every token queued (alive-first TopK, or exact scores asked for): GX_TB tokens a pass.
+template <typename E, bool ALIVE>
+__global__ void __launch_bounds__(GX_NT) gate_exact_kernel(GateArgs a, const int32_t* queue) {
+  __shared__ double s64[GX_TB][DM_MAX];
+  __shared__ double sd[GX_TB][DM_MAX];
+  __shared__ uint8_t alv[ALIVE ? NMAX : 1];                          // alive flags (ALIVE ranking)
+  exact_body<E, ALIVE, GX_TB>(a, queue, s64, sd, alv);
+}
+
+// The tokens the certificate rejects (bf16 MFMA scores): one token a pass, two blocks
+// per compute unit.
+__global__ void __launch_bounds__(GX_NT) __attribute__((amdgpu_waves_per_eu(4)))
+gate_exact_sparse_kernel(GateArgs a, const int32_t* queue) {
+  __shared__ double s64[1][DM_MAX];
+  __shared__ double sd[1][DM_MAX];
+  exact_body<bf16, false, 1>(a, queue, s64, sd, nullptr);
 }
 
 // every token into the queue (the exact path for all of them)
@@ -731,7 +895,7 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
     if (!aligned16(ws)) return DMOE_EUNSUPPORTED;
     int32_t* queue = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + workspace_layout(s).gq_off);
     hipLaunchKernelGGL(gate_queue_all, dim3((unsigned)((s.T + 255) / 256)), dim3(256), 0, st, queue, (int)s.T);
-    const int xgrid = (int)std::min<int64_t>(s.T, 2048);
+    const int xgrid = (int)std::min<int64_t>((s.T + GX_TB - 1) / GX_TB, 1024);
     if (s.dtype == DMOE_BF16)
       hipLaunchKernelGGL((gate_exact_kernel<bf16, true>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
     else
@@ -758,8 +922,13 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
     const dim3 grid((unsigned)((s.T + GM_TOK - 1) / GM_TOK));
     hipLaunchKernelGGL(kern, grid, dim3(GM_NT), lds, st, ga);
     // exact recomputation of the queued tokens: persistent blocks over the queue
-    const int xgrid = (int)std::min<int64_t>(s.T, 1024);
-    hipLaunchKernelGGL((gate_exact_kernel<bf16, false>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+    if (s.flags & DMOE_FLAG_GATE_EXACT) {
+      const int xgrid = (int)std::min<int64_t>((s.T + GX_TB - 1) / GX_TB, 1024);
+      hipLaunchKernelGGL((gate_exact_kernel<bf16, false>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+    } else {
+      const int xgrid = (int)std::min<int64_t>(s.T, 1024);
+      hipLaunchKernelGGL(gate_exact_sparse_kernel, dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+    }
   } else {
     // fp32, and bf16 with more than 96 gate columns: exact fp64 scores for every token
     const dim3 grid((unsigned)((s.T + GATE_TB - 1) / GATE_TB));
