@@ -290,9 +290,12 @@ __global__ void __launch_bounds__(GATE_NT) gate_topk_kernel(GateArgs a) {
 // queue and recomputed with exact fp64 accumulation by gate_exact_kernel.
 
 constexpr int GM_TOK = 32;        // tokens per block (one MFMA row block)
-constexpr int GM_KW = 2;          // waves per block, each a share of the d_model groups
-constexpr int GM_NT = 64 * GM_KW;
-constexpr int GM_RING = 4;        // x groups (32 tokens x 64 d_model, 4 KB) in flight per wave
+constexpr int GM_RING = 2;        // x groups (32 tokens x 64 d_model, 4 KB) in flight per wave
+// Waves per block (each a share of the d_model groups): 2 from d_model 2048 on, else 1.
+// A 2-slot ring keeps a block's LDS small (8 KB per slot and wave with 32 gate columns),
+// so that several blocks share a compute unit and one block's selection overlaps the
+// others' loads.
+constexpr int gm_kw(int64_t D) { return D >= 2048 ? 2 : 1; }
 constexpr int GX_NT = 512;        // exact recomputation: threads per token
 
 struct GateMfmaArgs {
@@ -307,8 +310,8 @@ __device__ __forceinline__ void g2l16(const void* g, void* lds_wave_base) {
                                    (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0, 0);
 }
 
-// A block of GM_KW waves scores 32 tokens against all d*M gate columns; wave w takes
-// the d_model groups w, w + GM_KW, ... (groups of 64 values).  x and Wg stream
+// A block of KW waves scores 32 tokens against all d*M gate columns; wave w takes
+// the d_model groups w, w + KW, ... (groups of 64 values).  x and Wg stream
 // through a per-wave LDS ring of GM_RING groups (direct global->LDS loads, 8 rows x
 // 128 bytes per instruction, 16-byte chunks XOR-swizzled by row): a slot holds 32
 // token rows, then 32*CB gate-column rows.  Within a group, lane half h holds
@@ -316,8 +319,8 @@ __device__ __forceinline__ void g2l16(const void* g, void* lds_wave_base) {
 // operands (the contraction order is permuted identically for x and Wg).  The
 // waves' fp64 partial sums are added in wave order in LDS, then one lane per token
 // selects.
-template <int CB>                      // 32-column blocks of the d*M gate columns
-__global__ void __launch_bounds__(GM_NT) gate_topk_mfma(GateMfmaArgs ga) {
+template <int CB, int KW>              // 32-column blocks of the d*M gate columns; waves
+__global__ void __launch_bounds__(64 * KW) gate_topk_mfma(GateMfmaArgs ga) {
   const GateArgs& a = ga.a;
   extern __shared__ __align__(1024) unsigned char sm[];
   constexpr int SLOT = 4096 * (1 + CB);          // bytes per ring slot
@@ -337,14 +340,14 @@ __global__ void __launch_bounds__(GM_NT) gate_topk_mfma(GateMfmaArgs ga) {
   const bf16* bg = reinterpret_cast<const bf16*>(a.bg);
   const int tok = lane & 31, half = lane >> 5;
   const int NG = a.D / 64;
-  const int ng = NG > wv ? (NG - wv + GM_KW - 1) / GM_KW : 0;   // groups of this wave
+  const int ng = NG > wv ? (NG - wv + KW - 1) / KW : 0;         // groups of this wave
   char* ring = reinterpret_cast<char*>(sm) + wv * (GM_RING * SLOT);
   // instruction q fills rows 8q .. 8q+7 of the slot (q < 4: tokens, then gate columns);
   // lane -> row 8q + lane/8, chunk lane%8 stored at position (lane%8) ^ (row%8)
   const int lrow = lane >> 3, lch = lane & 7;
   auto issue = [&](int m) {                       // the wave's m-th group
     char* slot = ring + (m % GM_RING) * SLOT;
-    const int64_t k0 = (int64_t)64 * (wv + GM_KW * m);
+    const int64_t k0 = (int64_t)64 * (wv + KW * m);
 #pragma unroll
     for (int q = 0; q < 4 * (1 + CB); ++q) {
       const int r = 8 * q + lrow;
@@ -420,7 +423,7 @@ __global__ void __launch_bounds__(GM_NT) gate_topk_mfma(GateMfmaArgs ga) {
   const int SLD = dM + 1;
   double* s64 = reinterpret_cast<double*>(sm);                 // [32][SLD]
   float* ab = reinterpret_cast<float*>(s64 + GM_TOK * SLD);    // [32][SLD]
-  for (int w = 0; w < GM_KW; ++w) {
+  for (int w = 0; w < KW; ++w) {
     if (wv == w) {
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb) {
@@ -776,8 +779,8 @@ __global__ void gate_queue_all(int32_t* queue, int T) {
   if (i < T) queue[GQ_HEAD + i] = i;
 }
 
-static size_t gate_mfma_lds_bytes(int dM) {
-  const size_t ring = (size_t)GM_KW * GM_RING * 4096 * (1 + (dM + 31) / 32);
+static size_t gate_mfma_lds_bytes(int dM, int kw) {
+  const size_t ring = (size_t)kw * GM_RING * 4096 * (1 + (dM + 31) / 32);
   const size_t scores = (sizeof(double) + sizeof(float)) * GM_TOK * (dM + 1);
   return ring > scores ? ring : scores;
 }
@@ -911,16 +914,18 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
     const double gD = (double)s.D * u / (1 - (double)s.D * u);
     int32_t* queue = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + workspace_layout(s).gq_off);
     GateMfmaArgs ga{a, s.flags, (float)(g32 / (1 - gD) * 1.0001), queue};
-    const size_t lds = gate_mfma_lds_bytes((int)s.dM);
+    const int KW = gm_kw(s.D);
+    const size_t lds = gate_mfma_lds_bytes((int)s.dM, KW);
     const int CB = (int)((s.dM + 31) / 32);
-    auto kern = CB == 1 ? gate_topk_mfma<1> : CB == 2 ? gate_topk_mfma<2> : gate_topk_mfma<3>;
+    auto kern = KW == 2 ? (CB == 1 ? gate_topk_mfma<1, 2> : CB == 2 ? gate_topk_mfma<2, 2> : gate_topk_mfma<3, 2>)
+                        : (CB == 1 ? gate_topk_mfma<1, 1> : CB == 2 ? gate_topk_mfma<2, 1> : gate_topk_mfma<3, 1>);
     if (lds > 65536) {
       (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       (void)hipGetLastError();
     }
     fill_zero(queue, sizeof(int32_t), st);
     const dim3 grid((unsigned)((s.T + GM_TOK - 1) / GM_TOK));
-    hipLaunchKernelGGL(kern, grid, dim3(GM_NT), lds, st, ga);
+    hipLaunchKernelGGL(kern, grid, dim3(64 * KW), lds, st, ga);
     // exact recomputation of the queued tokens: persistent blocks over the queue
     if (s.flags & DMOE_FLAG_GATE_EXACT) {
       const int xgrid = (int)std::min<int64_t>((s.T + GX_TB - 1) / GX_TB, 1024);

@@ -253,7 +253,7 @@ dispatch_bwd_kernel(const E* dxp, const int32_t* pos, const int32_t* idx, const 
         }
       }
     }
-    *reinterpret_cast<uint4*>(dx + (int64_t)t * D + c * VEC) = Vec<E>::pack(acc);
+    store_stream16(dx + (int64_t)t * D + c * VEC, Vec<E>::pack(acc));
   }
 }
 

@@ -41,6 +41,10 @@ CASES = {
     # largest), 75 gate columns (three MFMA column blocks), 10% dead
     "bf16_maxgrid": Workload("bf16_maxgrid", 18, T=700, D=64, H=64, d=3, M=25, k=8, dtype="bf16",
                              act="gelu", p_alive=0.9),
+    # d_model >= 2048: the MFMA gate's two-wave blocks; 33 groups of 64 (one wave takes
+    # one group more), token count off the 32-token blocks
+    "bf16_wide_gate": Workload("bf16_wide_gate", 19, T=150, D=2112, H=64, d=2, M=16, k=4, dtype="bf16",
+                               act="gelu", p_alive=0.9),
 }
 
 
