@@ -43,14 +43,6 @@ template <typename E> __device__ __forceinline__ E cvt(float v);
 template <> __device__ __forceinline__ float cvt<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16 cvt<bf16>(float v) { return f2bf(v); }
 
-// 16-byte store with the non-temporal hint: for large outputs written once, so that
-// they do not stay in the caches as dirty lines that a later kernel's reads must first
-// write back.
-__device__ __forceinline__ void store_stream16(void* p, const uint4& v) {
-  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-  __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
-}
-
 // 16-byte vector of elements <-> 16/sizeof(E) floats
 template <typename E> struct Vec;
 template <> struct Vec<float> {

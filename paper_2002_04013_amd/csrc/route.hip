@@ -215,6 +215,15 @@ combine_bwd_kernel(const E* dy, const E* yp, const int32_t* pos, const float* w,
   }
 }
 
+// 16-byte store with the non-temporal hint, for large outputs written once in whole
+// 128-byte lines (a wave store covers 1 KB of one row): such lines are not left in the
+// caches as dirty lines that a later kernel's reads must first write back.  (Partial
+// lines written this way lose the caches' write combining.)
+__device__ __forceinline__ void store_stream16(void* p, const uint4& v) {
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
+}
+
 // dx[t] = sum_j dx_perm[pos[t,j]]  (+ sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])])
 template <typename E>
 __global__ void __launch_bounds__(RT_NT)
