@@ -269,15 +269,21 @@ def test_sgd_backward(name):
             assert np.median(np.abs(got[live] - old[live])) > 2 * np.median(_ulp(old[live], wl.dtype)), n
 
 
-@pytest.mark.parametrize("name", ["bf16_skew", "bf16_grid3d", "f32_grid4d", "few_alive"])
+@pytest.mark.parametrize("name", ["bf16_skew", "bf16_grid3d", "f32_grid4d", "few_alive", "bf16_maxgrid",
+                                  "alive_many"])
 def test_alive_topk(name):
     """DMOE_FLAG_ALIVE_TOPK: TopK among the alive experts (dead ones only to fill up
     when fewer than k respond), the whole layer forward and backward against the
     oracle's topk_alive_bruteforce routing; the chosen set differs from the plain
     TopK's on these partially alive grids."""
     from paper_2002_04013_amd.abi import DMOE_FLAG_ALIVE_TOPK
-    wl = CASES.get(name) or Workload("few_alive", 30, T=160, D=64, H=64, d=2, M=8, k=4, dtype="bf16",
-                                     act="gelu", p_alive=0.05)
+    # alive_many: more 8-token passes than blocks (every block loops), half the grid alive
+    wl = CASES.get(name) or {
+        "few_alive": Workload("few_alive", 30, T=160, D=64, H=64, d=2, M=8, k=4, dtype="bf16", act="gelu",
+                              p_alive=0.05),
+        "alive_many": Workload("alive_many", 31, T=8300, D=64, H=64, d=2, M=8, k=4, dtype="bf16", act="relu",
+                               p_alive=0.5),
+    }[name]
     say(f"[parity] alive TopK {name}")
     inp = make_inputs(wl, "cpu")
     if name == "few_alive":
