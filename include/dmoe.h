@@ -101,8 +101,9 @@ const char* dmoe_strerror(int code);
  * tie is recomputed with exact fp64 accumulation, so the selection equals the one
  * of the exact scores; the returned scores, g and w carry the (bounded) MFMA error.
  * fp32, and bf16 with d*M > 96: exact fp64 accumulation for every token.
- * Uses workspace: bf16 with d*M <= 96 yes (the queue of tokens to recompute; ws must
- * not be NULL), otherwise no. */
+ * Uses workspace: bf16 with d*M <= 96, and DMOE_FLAG_ALIVE_TOPK with either dtype
+ * (the queue of tokens to recompute; ws must not be NULL, else DMOE_EINVAL);
+ * otherwise no. */
 int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* Wg, const void* bg,
                    const uint8_t* alive, int32_t* idx, float* w, float* g, float* scores,
                    void* ws, void* stream);

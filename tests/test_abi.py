@@ -117,3 +117,15 @@ def test_new_entry_points_validate_on_host(lib):
     assert lib.workspace_bytes(lib.make_dims(64, 64, 1 << 23, 2, 4, 2)) == 0
     # unknown flag bits
     assert lib.workspace_bytes(lib.make_dims(64, 64, 256, 2, 4, 2, flags=4)) == 0
+
+
+def test_gate_workspace_required_on_host(lib):
+    """The gate's queue of tokens to recompute lives in the workspace: the MFMA path
+    (bf16, d*M <= 96) and the alive-first TopK (either dtype) reject ws = NULL before
+    any device work."""
+    raw = lib.load()
+    F = lambda: ctypes.c_void_p(1 << 20)
+    for dt, flags in (("bf16", 0), ("bf16", lib.DMOE_FLAG_ALIVE_TOPK), ("f32", lib.DMOE_FLAG_ALIVE_TOPK)):
+        dims = lib.make_dims(64, 64, 256, 2, 4, 2, dt, "relu", flags)
+        rc = raw.dmoe_gate_topk(ctypes.byref(dims), F(), F(), None, None, F(), F(), None, None, None, None)
+        assert rc == -1, (dt, flags)
