@@ -791,44 +791,78 @@ static size_t gate_lds_bytes(int dM) {
 
 // ---------------------------------------------------------------- backward
 
+constexpr int GD_NT = 128;         // gate backward: tokens per block
+
 // dg[t,j] = w (dw - sum_l w_l dw_l) over alive chosen experts; ds row t gets dg at
 // column i*M + u_i for every dimension i.  bf16: ds stores hi and lo bf16 parts
 // (columns [0, dM) and [dM, 2dM)) so the MFMA product keeps ~16 mantissa bits.
+
 template <typename E>
-__global__ void gate_dg_kernel(const int32_t* idx, const float* w, const float* dw,
-                               const uint8_t* alive, float* dg, E* ds, int64_t ds_ld,
-                               int T, int d, int M, int k, int dM) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= T) return;
-  float wv[KMAX], dv[KMAX];
-  int id[KMAX];
-  float s = 0.f;
-  for (int j = 0; j < k; ++j) {
-    id[j] = idx[(int64_t)t * k + j];
-    const bool live = alive == nullptr || alive[id[j]] != 0;
-    wv[j] = live ? w[(int64_t)t * k + j] : 0.f;
-    dv[j] = dw[(int64_t)t * k + j];
-    s = fmaf(wv[j], dv[j], s);
-  }
-  float row[DM_MAX];
+__global__ void __launch_bounds__(GD_NT)
+gate_dg_kernel(const int32_t* idx, const float* w, const float* dw, const uint8_t* alive, float* dg, E* ds,
+               int64_t ds_ld, int T, int d, int M, int k, int dM, float* dbg_part) {
+  // One thread per token builds its ds row (fp32, in LDS: rows of dM + 1 words); the
+  // block then writes its rows (consecutive tokens, one contiguous range) in 16-byte
+  // chunks, and adds each column over its rows in row order for the bias gradient.
+  extern __shared__ float rowbuf[];
+  constexpr int VEC = 16 / sizeof(E);
+  const int tl = threadIdx.x;
+  const int t0 = blockIdx.x * GD_NT, t = t0 + tl;
+  const int nt = min(GD_NT, T - t0);
+  const int SR = dM + 1;
+  float* row = rowbuf + tl * SR;
   for (int c = 0; c < dM; ++c) row[c] = 0.f;
-  for (int j = 0; j < k; ++j) {
-    const float gj = wv[j] * (dv[j] - s);
-    dg[(int64_t)t * k + j] = gj;
-    int rem = id[j];
-    for (int i = d - 1; i >= 0; --i) { row[i * M + rem % M] += gj; rem /= M; }
-  }
-  E* out = ds + (int64_t)t * ds_ld;
-  if constexpr (sizeof(E) == 2) {
-    for (int c = 0; c < dM; ++c) {
-      const bf16 hi = f2bf(row[c]);
-      out[c] = hi;
-      out[dM + c] = f2bf(row[c] - bf2f(hi));
+  if (t < T) {
+    float wv[KMAX], dv[KMAX];
+    int id[KMAX];
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      wv[j] = 0.f; dv[j] = 0.f; id[j] = 0;
+      if (j < k) {
+        id[j] = idx[(int64_t)t * k + j];
+        const bool live = alive == nullptr || alive[id[j]] != 0;
+        wv[j] = live ? w[(int64_t)t * k + j] : 0.f;
+        dv[j] = dw[(int64_t)t * k + j];
+        s = fmaf(wv[j], dv[j], s);
+      }
     }
-    for (int c = 2 * dM; c < ds_ld; ++c) out[c] = 0;
-  } else {
-    for (int c = 0; c < dM; ++c) out[c] = row[c];
-    for (int c = dM; c < ds_ld; ++c) out[c] = 0.f;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j < k) {
+        const float gj = wv[j] * (dv[j] - s);
+        dg[(int64_t)t * k + j] = gj;
+        int rem = id[j];
+        for (int i = d - 1; i >= 0; --i) { row[i * M + rem % M] += gj; rem /= M; }
+      }
+    }
+  }
+  __syncthreads();
+  // bf16: hi parts in columns [0, dM), lo parts in [dM, 2 dM), zeros up to ds_ld
+  const int cpr = (int)(ds_ld / VEC);
+  for (int q = tl; q < nt * cpr; q += GD_NT) {
+    const int r = q / cpr, cb = q % cpr;
+    const float* src = rowbuf + r * SR;
+    alignas(16) E v[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const int c = cb * VEC + e;
+      if constexpr (sizeof(E) == 2) {
+        if (c < dM) v[e] = f2bf(src[c]);
+        else if (c < 2 * dM) { const float a = src[c - dM]; v[e] = f2bf(a - bf2f(f2bf(a))); }
+        else v[e] = 0;
+      } else {
+        v[e] = c < dM ? src[c] : 0.f;
+      }
+    }
+    *reinterpret_cast<uint4*>(ds + (int64_t)(t0 + r) * ds_ld + cb * VEC) = *reinterpret_cast<const uint4*>(v);
+  }
+  if (dbg_part) {
+    for (int c = tl; c < dM; c += GD_NT) {
+      float a = 0.f;
+      for (int r = 0; r < nt; ++r) a += rowbuf[r * SR + c];
+      dbg_part[(int64_t)blockIdx.x * dM + c] = a;
+    }
   }
 }
 
@@ -857,20 +891,19 @@ __global__ void gate_reduce_kernel(const float* part, int nsplit, int64_t rows, 
   dWg[q] = cvt<E>(s);
 }
 
-// dbg[c] = sum_t ds[t][c] (fixed order: per-thread strided sums, then a tree)
+// dbg[c] = sum over the token blocks of their partial column sums, in block order:
+// thread i adds a contiguous run of blocks, then a tree over the threads.
 template <typename E>
-__global__ void gate_dbg_kernel(const E* ds, int64_t ds_ld, int T, int dM, E* dbg) {
+__global__ void __launch_bounds__(256) gate_dbg_kernel(const float* part, int nblk, int dM, E* dbg) {
   const int c = blockIdx.x;
+  const int per = (nblk + 255) / 256;
+  const int b0 = threadIdx.x * per, b1 = min(nblk, b0 + per);
   float s = 0.f;
-  for (int t = threadIdx.x; t < T; t += blockDim.x) {
-    const E* r = ds + (int64_t)t * ds_ld;
-    s += ldf(r + c);
-    if constexpr (sizeof(E) == 2) s += ldf(r + dM + c);
-  }
+  for (int b = b0; b < b1; ++b) s += part[(int64_t)b * dM + c];
   __shared__ float red[256];
   red[threadIdx.x] = s;
   __syncthreads();
-  for (int o = blockDim.x / 2; o > 0; o >>= 1) {
+  for (int o = 128; o > 0; o >>= 1) {
     if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
     __syncthreads();
   }
@@ -955,8 +988,17 @@ static int gate_bwd_impl(const Shape& s, const void* x, const int32_t* idx, cons
   int32_t* offs = reinterpret_cast<int32_t*>(base + L.tiles_off);
   int32_t* tpre = offs + (L.gsplit + 1);
   const int T = (int)s.T, D = (int)s.D, dM = (int)s.dM;
-  hipLaunchKernelGGL(gate_dg_kernel<E>, dim3((T + 127) / 128), dim3(128), 0, st, idx, w, dw, alive,
-                     dg, ds, L.ds_ld, T, s.d, s.M, s.k, dM);
+  // the bias gradient's per-block column sums use the forward pass's queue region
+  // (calls on one stream do not overlap): ceil(T / 128) x dM floats <= 4 T bytes
+  const int gblk = (T + GD_NT - 1) / GD_NT;
+  float* dbg_part = dbg ? reinterpret_cast<float*>(base + L.gq_off) : nullptr;
+  const size_t dg_lds = (size_t)GD_NT * (dM + 1) * sizeof(float);
+  if (dg_lds > 65536) {
+    (void)hipFuncSetAttribute((const void*)gate_dg_kernel<E>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dg_lds);
+    (void)hipGetLastError();
+  }
+  hipLaunchKernelGGL(gate_dg_kernel<E>, dim3(gblk), dim3(GD_NT), dg_lds, st, idx, w, dw, alive, dg, ds, L.ds_ld, T,
+                     s.d, s.M, s.k, dM, dbg_part);
   // dWg partials: one GROUP_K GEMM group per token split, C[split] = ds_split^T x_split
   constexpr int BM = 64, BN = 128, BK = 32, WM = 2, WN = 2;
   const int rows = (int)L.ds_ld;                     // GEMM M (ds columns incl. lo part/padding)
@@ -979,8 +1021,7 @@ static int gate_bwd_impl(const Shape& s, const void* x, const int32_t* idx, cons
   hipLaunchKernelGGL(gate_reduce_kernel<E>, dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, st,
                      part, (int)L.gsplit, (int64_t)rows, dM, D, reinterpret_cast<E*>(dWg));
   if (dbg)
-    hipLaunchKernelGGL(gate_dbg_kernel<E>, dim3(dM), dim3(256), 0, st, ds, L.ds_ld, T, dM,
-                       reinterpret_cast<E*>(dbg));
+    hipLaunchKernelGGL(gate_dbg_kernel<E>, dim3(dM), dim3(256), 0, st, dbg_part, gblk, dM, reinterpret_cast<E*>(dbg));
   return launch_status();
 }
 
