@@ -378,11 +378,8 @@ __global__ void __launch_bounds__(64 * KW) gate_topk_mfma(GateMfmaArgs ga) {
     // Vector-memory operations retire in issue order, and group m is followed by the
     // groups issued after it, LPG loads each: once at most that many are
     // outstanding, group m has landed.
-    const int after = min(GM_RING - 1, ng - 1 - m);
-    const int n = LPG * after;
-    if (n >= 48) wait_vmcnt<48>(); else if (n >= 36) wait_vmcnt<36>(); else if (n >= 32) wait_vmcnt<32>();
-    else if (n >= 24) wait_vmcnt<24>(); else if (n >= 16) wait_vmcnt<16>(); else if (n >= 12) wait_vmcnt<12>();
-    else if (n >= 8) wait_vmcnt<8>(); else wait_vmcnt<0>();
+    static_assert(GM_RING == 2, "one group in flight behind the current one");
+    if (m + 1 < ng) wait_vmcnt<LPG>(); else wait_vmcnt<0>();
     f32x16_t c[CB];
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb)

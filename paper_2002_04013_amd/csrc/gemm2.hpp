@@ -352,10 +352,17 @@ grouped_gemm2(GemmArgs<bf16> p) {
           mm(kk & 1);
           interleave();
         }
-        // stages issued after kt+1: up to kt+STAGES-1, capped by the last stage; the
-        // previous epilogue's stores come after the prologue stages 0..STAGES-1
-        const int last = kt + STAGES - 1 < nk - 1 ? kt + STAGES - 1 : nk - 1;
-        wait_stage(last - (kt + 1), kt + 1 < STAGES ? prev_stores : 0);
+        if constexpr (STAGES == 2) {
+          // stage kt+1 is the newest load stage; only at kt = 0 do the previous
+          // epilogue's stores follow it (a compile-time wait in the steady state)
+          if (kt == 0) wait_vmcnt_rt(prev_stores);
+          else wait_vmcnt<0>();
+        } else {
+          // stages issued after kt+1: up to kt+STAGES-1, capped by the last stage; the
+          // previous epilogue's stores come after the prologue stages 0..STAGES-1
+          const int last = kt + STAGES - 1 < nk - 1 ? kt + STAGES - 1 : nk - 1;
+          wait_stage(last - (kt + 1), kt + 1 < STAGES ? prev_stores : 0);
+        }
         fix_tail(t, kt + 1);
         block_sync_lds();               // every wave is done with slot kt and sees stage kt+1
         if (kt + STAGES < nk) issue(t, kt + STAGES);
