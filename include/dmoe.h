@@ -101,6 +101,8 @@ const char* dmoe_strerror(int code);
  * tie is recomputed with exact fp64 accumulation, so the selection equals the one
  * of the exact scores; the returned scores, g and w carry the (bounded) MFMA error.
  * fp32, and bf16 with d*M > 96: exact fp64 accumulation for every token.
+ * Inputs are expected to be finite: with NaN or infinite scores the choice is
+ * unspecified (every returned index is still a valid expert id) and w may be NaN.
  * Uses workspace: bf16 with d*M <= 96, and DMOE_FLAG_ALIVE_TOPK with either dtype
  * (the queue of tokens to recompute; ws must not be NULL, else DMOE_EINVAL);
  * otherwise no. */
