@@ -298,3 +298,30 @@ def test_alive_topk(name):
     live = inp["alive"].numpy().astype(bool)
     chosen_live = live[gpu["idx"].numpy()].sum(axis=1)
     assert (chosen_live == min(wl.k, int(live.sum()))).all()
+
+
+@pytest.mark.parametrize("flags", [0, 2])
+def test_non_finite_inputs_keep_indices_valid(flags):
+    """Tokens whose x holds NaN or infinities get an unspecified choice, but every
+    index stays a valid expert id and the dispatch stays consistent; the other tokens
+    are routed as usual."""
+    wl = CASES["bf16_skinny"]
+    say(f"[parity] non-finite inputs, flags={flags}")
+    inp = make_inputs(wl, "cpu")
+    x = inp["x"].clone()
+    x[3, 5] = float("nan")
+    x[10, :] = float("inf")
+    x[11, 0] = -float("inf")
+    inp["x"] = x
+    gpu = gpu_run(wl, inp, backward=False, flags=flags)
+    idx = gpu["idx"].numpy()
+    assert idx.min() >= 0 and idx.max() < wl.N
+    counts = gpu["counts"].numpy()
+    offsets = gpu["offsets"].numpy()
+    assert offsets[0] == 0 and np.all(np.diff(offsets) == counts)
+    clean = inp.copy()
+    clean["x"] = make_inputs(wl, "cpu")["x"]
+    ref = gpu_run(wl, clean, backward=False, flags=flags)
+    keep = np.ones(wl.T, bool)
+    keep[[3, 10, 11]] = False
+    np.testing.assert_array_equal(idx[keep], ref["idx"].numpy()[keep])
