@@ -7,7 +7,8 @@
 //      expert's first row (a scan down each column), the counts, and the offsets
 //      (an exclusive scan of the counts);
 //   3. each block ranks its pairs within every expert in pair order (wave-wide
-//      rank by lane comparison, waves taken in order) and writes pos/row_token;
+//      rank from one ballot per bit of the expert id, waves taken in order) and
+//      writes pos/row_token;
 //   4. each token's row of x is copied to its alive pairs' rows of x_perm.
 #include "common.hpp"
 
@@ -95,6 +96,7 @@ dispatch_scatter(const int32_t* idx, const uint8_t* alive, int P, int N, int k,
   for (int e = threadIdx.x; e < N; e += RT_NT) base[e] = offsets[e] + bh[e];
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nbits = 32 - __builtin_clz((unsigned)N);              // bits of the largest expert id
   for (int r = 0; r < DISP_CHUNK / RT_NT; ++r) {
     const int p = blockIdx.x * DISP_CHUNK + r * RT_NT + threadIdx.x;
     int e = -1;
@@ -102,15 +104,20 @@ dispatch_scatter(const int32_t* idx, const uint8_t* alive, int P, int N, int k,
       const int e0 = idx[p];
       if (alive == nullptr || alive[e0]) e = e0;
     }
-    int rank = 0;
-    bool last = true;
-    for (int s = 0; s < 64; ++s) {
-      const int o = __builtin_amdgcn_readlane(e, s);
-      if (o == e) {
-        rank += s < lane;
-        last = last && !(s > lane);
-      }
+    // lanes of this wave holding the same id (or both none): the intersection, over the
+    // id's bits and its sign, of the ballots of lanes that agree with this lane's bit
+    uint64_t same = ~0ull;
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = (e >> b) & 1;
+      const uint64_t on = __ballot(bit);
+      same &= bit ? on : ~on;
     }
+    {
+      const uint64_t neg = __ballot(e < 0);
+      same &= e < 0 ? neg : ~neg;
+    }
+    const int rank = __popcll(same & ((1ull << lane) - 1ull));
+    const bool last = ((same >> lane) >> 1) == 0ull;
     int row = -1;
     for (int w = 0; w < RT_NT / 64; ++w) {
       if (wave == w && e >= 0) {
