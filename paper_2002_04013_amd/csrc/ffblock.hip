@@ -131,8 +131,10 @@ ln_act_fwd_kernel(const E* h, const int32_t* offsets, int N, int F, const E* gam
 // Input gradient of the normalisation step, per row:
 //   n = (h - mean) rstd, z = g n + b, dn = da act'(z) g,
 //   dh = rstd (dn - mean_f(dn) - n mean_f(dn n)).
-// The whole row is read before it is written, so dh may alias da.  As in the forward,
-// the next row is loaded before this row is stored, and g, b stay in registers.
+// The whole row is read before it is written, so dh may alias da.  dn is kept in fp32
+// registers between the two passes (the second pass only recomputes n); g and b are
+// read per chunk (the expert's two rows stay in L1), so that several waves share a
+// SIMD and one wave's arithmetic covers another's loads.
 template <typename E, int CH, int ACT>
 __global__ void __launch_bounds__(LN_NT)
 ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, int N, int F, const E* gamma,
@@ -145,45 +147,39 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
   const float invF = 1.f / (float)F;
   int e = row_expert(offsets, N, rr.r0);
   int eend = offsets[e + 1];
-  int eg = -1;
-  uint4 hv[CH], dv[CH], gv[CH], bv[CH];
-  auto load_row = [&](uint4 (&v)[CH], const E* src) {
+  for (int r = rr.r0; r < rr.r1; ++r) {
+    while (r >= eend) eend = offsets[++e + 1];
+    const E* gr = gamma + (int64_t)e * F;
+    const E* br = beta + (int64_t)e * F;
+    uint4 hv[CH], dv[CH];
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int c = lane + 64 * i;
-      v[i] = c < nch ? *reinterpret_cast<const uint4*>(src + c * VEC) : make_uint4(0, 0, 0, 0);
-    }
-  };
-  load_row(hv, h + (int64_t)rr.r0 * F);
-  load_row(dv, da + (int64_t)rr.r0 * F);
-  for (int r = rr.r0; r < rr.r1; ++r) {
-    while (r >= eend) eend = offsets[++e + 1];
-    if (e != eg) {
-      load_row(gv, gamma + (int64_t)e * F);
-      load_row(bv, beta + (int64_t)e * F);
-      eg = e;
-    }
-    uint4 hn[CH], dn_[CH];
-    if (r + 1 < rr.r1) {
-      load_row(hn, h + (int64_t)(r + 1) * F);
-      load_row(dn_, da + (int64_t)(r + 1) * F);
+      hv[i] = c < nch ? *reinterpret_cast<const uint4*>(h + (int64_t)r * F + c * VEC) : make_uint4(0, 0, 0, 0);
+      dv[i] = c < nch ? *reinterpret_cast<const uint4*>(da + (int64_t)r * F + c * VEC) : make_uint4(0, 0, 0, 0);
     }
     const float2 st = *reinterpret_cast<const float2*>(stats + 2 * (int64_t)r);
     const float mean = st.x, rstd = st.y;
+    float dnf[CH][VEC];
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int c = lane + 64 * i;
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) dnf[i][j] = 0.f;
       if (c >= nch) continue;
+      const uint4 gq = *reinterpret_cast<const uint4*>(gr + c * VEC);
+      const uint4 bq = *reinterpret_cast<const uint4*>(br + c * VEC);
       float x[VEC], d[VEC], g[VEC], b[VEC];
       Vec<E>::unpack(hv[i], x);
       Vec<E>::unpack(dv[i], d);
-      Vec<E>::unpack(gv[i], g);
-      Vec<E>::unpack(bv[i], b);
+      Vec<E>::unpack(gq, g);
+      Vec<E>::unpack(bq, b);
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
         const float n = (x[j] - mean) * rstd;
         const float dn = d[j] * act_b<E, ACT>(fmaf(g[j], n, b[j])) * g[j];
+        dnf[i][j] = dn;
         s1 += dn;
         s2 += dn * n;
       }
@@ -194,22 +190,14 @@ ln_act_bwd_rows_kernel(const E* h, const float* stats, const int32_t* offsets, i
     for (int i = 0; i < CH; ++i) {
       const int c = lane + 64 * i;
       if (c >= nch) continue;
-      float x[VEC], d[VEC], g[VEC], b[VEC], o[VEC];
+      float x[VEC], o[VEC];
       Vec<E>::unpack(hv[i], x);
-      Vec<E>::unpack(dv[i], d);
-      Vec<E>::unpack(gv[i], g);
-      Vec<E>::unpack(bv[i], b);
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
         const float n = (x[j] - mean) * rstd;
-        const float dn = d[j] * act_b<E, ACT>(fmaf(g[j], n, b[j])) * g[j];
-        o[j] = rstd * (dn - m1 - n * m2);
+        o[j] = rstd * (dnf[i][j] - m1 - n * m2);
       }
       *reinterpret_cast<uint4*>(out + c * VEC) = Vec<E>::pack(o);
-    }
-    if (r + 1 < rr.r1) {
-#pragma unroll
-      for (int i = 0; i < CH; ++i) { hv[i] = hn[i]; dv[i] = dn_[i]; }
     }
   }
 }
