@@ -289,6 +289,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in evs) / args.steps for n in timed}
+    # per-step device time (first call's start to last call's end event of each step)
+    per_step = sorted(e[timed[0]][0].elapsed_time(e[timed[-1]][1]) for e in evs)
     print(f"[bench] {args.steps} steps in {wall:.3f} s; per call ms: " +
           ", ".join(f"{n} {v:.3f}" for n, v in ms.items()), file=sys.stderr, flush=True)
 
@@ -341,6 +343,8 @@ def main():
         "gate_topk": roof("gate_topk"),
         "dispatch": roof("dispatch"),
         "calls_ms": {n: round(v, 4) for n, v in ms.items()},
+        "step_ms": {"median": round(per_step[len(per_step) // 2], 3), "min": round(per_step[0], 3),
+                    "max": round(per_step[-1], 3)},
     }
     if not args.no_cpu_baseline:
         host = {n: v for n, v in inp.items()}
