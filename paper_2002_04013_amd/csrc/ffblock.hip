@@ -556,7 +556,7 @@ extern "C" int dmoe_expert_ffblock_bwd(const dmoe_dims* dims, const int32_t* off
       block_bwd<bf16, G2Fat, G2DW>(s, offsets, c(x_perm), params_of<bf16>(params), acts_of<bf16>(acts), c(dy_perm),
                                    m(g1), m(g2), m(dx_perm), grads_of<bf16>(grads), tpre, st);
     else
-      block_bwd<bf16, G2Skinny, G2DW>(s, offsets, c(x_perm), params_of<bf16>(params), acts_of<bf16>(acts),
+      block_bwd<bf16, G2Skinny, G2DWShort>(s, offsets, c(x_perm), params_of<bf16>(params), acts_of<bf16>(acts),
                                       c(dy_perm), m(g1), m(g2), m(dx_perm), grads_of<bf16>(grads), tpre, st);
   } else {
     auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };

@@ -323,7 +323,7 @@ extern "C" int dmoe_expert_ffn_bwd(const dmoe_dims* dims, const int32_t* offsets
       ffn_bwd_bf16<G2Fat, G2DW>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
                                 m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
     else
-      ffn_bwd_bf16<G2Skinny, G2DW>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
+      ffn_bwd_bf16<G2Skinny, G2DWShort>(s, offsets, c(x_perm), c(h), c(a), c(dy_perm), c(W1), c(W2), m(dh),
                                    m(dx_perm), m(dW1), m(db1), m(dW2), m(db2), tpre, st);
   } else {
     auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };
@@ -392,7 +392,7 @@ extern "C" int dmoe_expert_ffn_bwd_sgd(const dmoe_dims* dims, const int32_t* off
       ffn_bwd_sgd_bf16<G2Fat, G2DW>(s, offsets, c(x_perm), c(a), c(dy_perm), m(W1), m(b1), m(W2), m(b2), lr,
                                     c(h), m(dh), m(dx_perm), tpre, st);
     else
-      ffn_bwd_sgd_bf16<G2Skinny, G2DW>(s, offsets, c(x_perm), c(a), c(dy_perm), m(W1), m(b1), m(W2), m(b2), lr,
+      ffn_bwd_sgd_bf16<G2Skinny, G2DWShort>(s, offsets, c(x_perm), c(a), c(dy_perm), m(W1), m(b1), m(W2), m(b2), lr,
                                        c(h), m(dh), m(dx_perm), tpre, st);
   } else {
     auto c = [](const void* q) { return reinterpret_cast<const float*>(q); };

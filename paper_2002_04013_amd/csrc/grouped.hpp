@@ -162,9 +162,14 @@ struct CfgDWF32  { static constexpr int BM = 64, BN = 64, BK = 32, WM = 2, WN = 
 // bf16 tile shapes of the gemm2 path: many rows per expert -> 256x256 tiles, 8 waves,
 // 64-deep k, 2 stages (best of the measured shapes at the wide workload for all three
 // operand layouts); few rows -> 32x256 tiles, 4 waves, 4 stages (weight streaming).
-struct G2Fat    { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
-struct G2Skinny { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4, BK = 64; };
-struct G2DW     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
+// Weight gradients contract over an expert's rows: 64-deep k-steps when experts hold
+// many rows, 32-deep ones when they hold few (a k-step past an expert's last row is
+// zero-filled in LDS and still multiplied, so with ~16 rows per expert a 64-deep step
+// spends three quarters of its MFMA and LDS reads on zeros).
+struct G2Fat     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
+struct G2Skinny  { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4, BK = 64; };
+struct G2DW      { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
+struct G2DWShort { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 4, BK = 32; };
 
 static bool use_fat(const Shape& s) { return s.P >= (int64_t)96 * s.N; }
 
