@@ -28,6 +28,10 @@ CASES = {
     # skewed gate as in the failure+skew workload, at a small size
     "bf16_skew": Workload("bf16_skew", 14, T=1024, D=256, H=256, d=2, M=16, k=4, dtype="bf16",
                           act="gelu", p_alive=0.9, gate_scale=4.0, skew_rows=4),
+    # the same skew at twice the tokens: 11 experts hold more than 128 rows (up to 301),
+    # so the few-rows weight-gradient GEMM (32-deep k-steps, 4 stages) wraps its ring
+    "bf16_skew_deep": Workload("bf16_skew_deep", 30, T=2048, D=128, H=256, d=2, M=16, k=4, dtype="bf16",
+                               act="gelu", p_alive=0.9, gate_scale=4.0, skew_rows=4),
     # 4-D grid, fp32
     "f32_grid4d": Workload("f32_grid4d", 15, T=200, D=64, H=64, d=4, M=3, k=5, dtype="f32",
                            act="gelu", p_alive=0.7),
@@ -218,7 +222,7 @@ def _ulp(ref, dtype):
     return 2.0 ** (e - bits + 1)
 
 
-@pytest.mark.parametrize("name", ["bf16_skinny", "bf16_fat", "f32_grid4d"])
+@pytest.mark.parametrize("name", ["bf16_skinny", "bf16_skew_deep", "bf16_fat", "f32_grid4d"])
 def test_sgd_backward(name):
     """dmoe_expert_ffn_bwd_sgd: dh and dx_perm bit-identical to the plain backward
     (computed from the parameters on entry); each parameter becomes
