@@ -96,14 +96,22 @@ segment_colsum(const E* X, int64_t ld, const int32_t* offsets, int ncols, E* out
   *op = Vec<E>::pack(acc);
 }
 
+constexpr int MAX_DEVICES = 64;
+
+// The current device, or -1 when it cannot be told or is beyond MAX_DEVICES.
+static int current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return -1;
+  return dev;
+}
+
 static int device_cus() {
-  static int cus[64] = {0};
-  int dev = 0;
-  hipGetDevice(&dev);
-  if (dev < 0 || dev >= 64) return 256;
+  static int cus[MAX_DEVICES] = {0};
+  const int dev = current_device();
+  if (dev < 0) return 256;
   if (!cus[dev]) {
     int v = 0;
-    hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev);
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) v = 0;
     cus[dev] = v > 0 ? v : 256;
   }
   return cus[dev];
@@ -115,13 +123,15 @@ static void run_gemm(GemmArgs<E> p, int64_t tiles_ub, hipStream_t st) {
   auto kern = grouped_gemm<E, GM, B_KC, EPI, BM, BN, BK, WM, WN>;
   constexpr int NT = 64 * WM * WN;
   const size_t lds = gemm_lds_bytes<E, BM, BN, BK, WM, WN>();
-  static int per_cu = 0;
-  if (!per_cu) {
-    int nb = 0;
+  static int per_cu[MAX_DEVICES] = {0};       // resident blocks per compute unit, per device
+  const int dev = current_device();
+  int nb = dev >= 0 ? per_cu[dev] : 0;
+  if (!nb) {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, NT, lds) != hipSuccess || nb < 1) nb = 1;
-    per_cu = nb;
+    (void)hipGetLastError();
+    if (dev >= 0) per_cu[dev] = nb;
   }
-  const int64_t resident = (int64_t)per_cu * device_cus();
+  const int64_t resident = (int64_t)nb * device_cus();
   const int grid = (int)std::min<int64_t>(tiles_ub, resident);
   p.chunked = grid >= 8;
   hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
@@ -134,15 +144,17 @@ static void run_gemm2(GemmArgs<bf16> p, int64_t tiles_ub, hipStream_t st) {
   auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1, BK>;
   constexpr int NT = 64 * WM * WN;
   const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT, BK>();
-  static int per_cu = 0;
-  if (!per_cu) {
+  static int per_cu[MAX_DEVICES] = {0};       // resident blocks per compute unit, per device
+  const int dev = current_device();
+  int nb = dev >= 0 ? per_cu[dev] : 0;
+  if (!nb) {
+    // dynamic LDS beyond 64 KiB is opted into per kernel, on the current device
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    int nb = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, NT, lds) != hipSuccess || nb < 1) nb = 1;
     (void)hipGetLastError();
-    per_cu = nb;
+    if (dev >= 0) per_cu[dev] = nb;
   }
-  const int64_t resident = (int64_t)per_cu * device_cus();
+  const int64_t resident = (int64_t)nb * device_cus();
   const int grid = (int)std::min<int64_t>(tiles_ub, resident);
   p.chunked = grid >= 8;
   hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
