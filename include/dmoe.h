@@ -28,6 +28,11 @@
  *   - Buffers are sized for P_max rows; the number of rows actually used,
  *     offsets[N], stays on the device (no host synchronisation on the path).
  *   - Results are bitwise reproducible from run to run (no floating-point atomics).
+   - Workspace contents need no initialisation: an entry point reads only workspace
+     memory it has written itself (counters are cleared by kernels, not memsets).
+   - The calls can be recorded into a HIP graph by stream capture and replayed (no
+     allocation, synchronisation or memset node); a replay computes what the eager
+     calls compute, bit for bit.
  *   - Supported: 1 <= d <= 4, 1 <= M, d*M <= 128, 1 <= k <= min(N, 8),
  *     N <= 16384, T >= 0, D and H multiples of 64 and at most 2^22, pointers 16-byte aligned.
  *
