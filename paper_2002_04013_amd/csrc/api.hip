@@ -24,7 +24,8 @@ int check_dims(const dmoe_dims* dims, Shape* s) {
   if (q.D % 64 || q.H % 64) return DMOE_EUNSUPPORTED;
   // tile loads address a tile's rows with 32-bit byte offsets (256 rows x ld x 2 bytes)
   if (q.D > (1 << 22) || q.H > (1 << 22)) return DMOE_EUNSUPPORTED;
-  if (q.T * q.k > (int64_t)0x7fffffff / 2) return DMOE_EUNSUPPORTED;
+  // pair and row indices are 32-bit (T * k rows, with headroom for tile rounding)
+  if (q.T > (int64_t)0x7fffffff || q.T * q.k > (int64_t)0x7fffffff / 2) return DMOE_EUNSUPPORTED;
   s->T = q.T; s->D = q.D; s->H = q.H; s->N = N; s->P = q.T * q.k; s->dM = (int64_t)q.d * q.M;
   s->d = q.d; s->M = q.M; s->k = q.k; s->dtype = q.dtype; s->act = q.act; s->flags = q.flags;
   s->esz = q.dtype == DMOE_BF16 ? 2 : 4;

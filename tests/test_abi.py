@@ -115,6 +115,10 @@ def test_new_entry_points_validate_on_host(lib):
     # widths past the 32-bit tile addressing limit
     assert lib.workspace_bytes(lib.make_dims(64, 1 << 23, 256, 2, 4, 2)) == 0
     assert lib.workspace_bytes(lib.make_dims(64, 64, 1 << 23, 2, 4, 2)) == 0
+    # token counts whose pair indices do not fit 32 bits (no overflow in the check itself)
+    assert lib.workspace_bytes(lib.make_dims(1 << 28, 64, 256, 2, 4, 4)) == 0
+    assert lib.workspace_bytes(lib.make_dims(1 << 62, 64, 256, 2, 4, 4)) == 0
+    assert lib.workspace_bytes(lib.make_dims((1 << 28) - 1, 64, 256, 2, 4, 4)) > 0
     # unknown flag bits
     assert lib.workspace_bytes(lib.make_dims(64, 64, 256, 2, 4, 2, flags=4)) == 0
 
