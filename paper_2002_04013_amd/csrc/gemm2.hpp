@@ -35,6 +35,22 @@ __device__ __forceinline__ void g2l_16(const void* g, void* lds_wave_base) {
 __device__ __forceinline__ void g2l_16_at(const bf16* base, uint32_t off_bytes, void* lds_wave_base) {
   g2l_16(reinterpret_cast<const char*>(base) + off_bytes, lds_wave_base);
 }
+// The same load written out as the instruction (M0 = the wave's LDS destination, one
+// wait state before the load reads it).  The compiler does not know it writes LDS, so
+// it adds no wait of its own for it: it would otherwise drain every outstanding
+// direct-to-LDS load (vmcnt(0)) before each transposing LDS read (ds_read_b64_tr_b16),
+// whose LDS operand it cannot tell apart from the loads' destinations, serialising
+// the ring.  The pipeline's own vmcnt waits and barriers order these loads.
+__device__ __forceinline__ void g2l_16_at_asm(const bf16* base, uint32_t off_bytes, void* lds_wave_base) {
+  const uint32_t m = (uint32_t)(uintptr_t)(lds_ptr_t)lds_wave_base;
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off_bytes), "s"(base), "s"(m) : "memory", "m0");
+}
+template <bool ASM>
+__device__ __forceinline__ void g2l_tile(const bf16* base, uint32_t off_bytes, void* lds_wave_base) {
+  if constexpr (ASM) g2l_16_at_asm(base, off_bytes, lds_wave_base);
+  else g2l_16_at(base, off_bytes, lds_wave_base);
+}
 
 // s_waitcnt vmcnt(n) with expcnt/lgkmcnt left free (gfx9 encoding).
 template <int N>
@@ -61,7 +77,7 @@ __device__ __forceinline__ int swz_kc(int r) {
 }
 
 // ---- K-contiguous tile [R][BK] -------------------------------------------------------
-template <int R, int NW, int SW, int BK>
+template <int R, int NW, int SW, int BK, bool ASM = false>
 struct KcTile {
   static constexpr int RB = BK * 2;                    // bytes per row
   static constexpr int CH = BK / 8;                    // chunks per row
@@ -81,7 +97,7 @@ struct KcTile {
       const int r = q * RPI + lane / CH;
       const int c = (lane % CH) ^ swz_kc<BK, SW>(r);
       const int rr = r < rvalid ? r : rvalid - 1;
-      g2l_16_at(base, ((uint32_t)rr * (uint32_t)ld + (uint32_t)(c * 8)) * 2u, lds + q * 1024);
+      g2l_tile<ASM>(base, ((uint32_t)rr * (uint32_t)ld + (uint32_t)(c * 8)) * 2u, lds + q * 1024);
     }
   }
   // fragment of rows r0 + (lane % 32), k chunk kc + lane / 32 (8 bf16)
@@ -93,7 +109,7 @@ struct KcTile {
 };
 
 // ---- N-contiguous tile [BK][R] (row = k) ---------------------------------------------
-template <int R, int NW, int BK>
+template <int R, int NW, int BK, bool ASM = false>
 struct NcTile {
   static constexpr int BYTES = BK * R * 2;
   static constexpr int CPR = R / 8;                    // chunks per row
@@ -115,7 +131,7 @@ struct NcTile {
       int col = c * 8;
       col = col < cvalid ? col : ((cvalid - 1) & ~7);
       const int kk = k < kvalid ? k : kvalid - 1;
-      g2l_16_at(base, ((uint32_t)kk * (uint32_t)ld + (uint32_t)col) * 2u, lds + q * 1024);
+      g2l_tile<ASM>(base, ((uint32_t)kk * (uint32_t)ld + (uint32_t)col) * 2u, lds + q * 1024);
     }
   }
   // zero rows [kvalid, BK) of the tile (GROUP_K tail)
@@ -146,6 +162,25 @@ struct NcTile {
     return __builtin_bit_cast(bf16x8_t, v);
   }
 };
+
+// The tile plan and the expert offsets are written by earlier kernels and only read
+// while a GEMM runs.  Read through the constant address space with wave-uniform
+// indices they become scalar loads, counted by lgkmcnt: they neither join the vector
+// memory queue whose in-order counts the pipeline waits on nor force it to drain.
+__device__ __forceinline__ int ld_plan(const int32_t* p, int i) {
+  return ((const __attribute__((address_space(4))) int32_t*)p)[i];
+}
+// expert owning global tile L (tiles of expert e start at tprefix[e] * scale), for a
+// tile not below the one whose expert was `hint`
+__device__ __forceinline__ int find_group_plan(const int32_t* tprefix, int scale, int groups, int L, int hint) {
+  if (ld_plan(tprefix, hint + 1) * scale > L) return hint;
+  int lo = hint + 1, hi = groups;   // tprefix[lo]*scale <= L < tprefix[hi]*scale
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (ld_plan(tprefix, mid) * scale <= L) lo = mid; else hi = mid;
+  }
+  return lo;
+}
 
 // Runtime-selected s_waitcnt vmcnt(n) for n in [0, 63] (n is wave-uniform).
 __device__ __forceinline__ void wait_vmcnt_rt(int n) {
@@ -182,8 +217,11 @@ grouped_gemm2(GemmArgs<bf16> p) {
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int KK = BK / 16;
-  using TA = typename std::conditional<A_T, NcTile<BM, NW, BK>, KcTile<BM, NW, SW, BK>>::type;
-  using TB = typename std::conditional<B_T, NcTile<BN, NW, BK>, KcTile<BN, NW, SW, BK>>::type;
+  // kernels with transposing LDS reads issue their direct-to-LDS loads as written-out
+  // instructions (see g2l_16_at_asm)
+  constexpr bool DMA_ASM = A_T || B_T;
+  using TA = typename std::conditional<A_T, NcTile<BM, NW, BK, DMA_ASM>, KcTile<BM, NW, SW, BK, DMA_ASM>>::type;
+  using TB = typename std::conditional<B_T, NcTile<BN, NW, BK, DMA_ASM>, KcTile<BN, NW, SW, BK, DMA_ASM>>::type;
   constexpr int ABYTES = TA::BYTES, SBYTES = TA::BYTES + TB::BYTES;
   constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave
   // store instructions of a full tile's epilogue, per wave
@@ -200,7 +238,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
 
-  const int total = p.tprefix[p.groups] * p.tscale;
+  const int total = ld_plan(p.tprefix, p.groups) * p.tscale;
   int L, Lend, Lstep;
   if (p.chunked) {
     const int x = blockIdx.x & 7, lb = blockIdx.x >> 3;
@@ -215,17 +253,29 @@ grouped_gemm2(GemmArgs<bf16> p) {
   // Coordinates and operand bases of tile L.
   struct TileC {
     int e, off, m0, n0, mvalid, nvalid, kvalid, nk;
+    int base;                      // ring slot of the tile's stage 0 (EARLY only; else 0)
     const bf16* Ab;
     const bf16* Bb;
+  };
+  // Weight-gradient GEMMs with a deep ring: when a tile has fewer k-steps than the ring
+  // has slots (few rows per expert), the next tile's first stages are loaded into the
+  // free slots before this tile's MFMAs, so their latency hides behind this tile's
+  // work and stores instead of being waited for right after them.  Stage s of a tile
+  // sits in slot (base + s) % STAGES, base following the previous tile's last stage.
+  constexpr bool EARLY = GM == GROUP_K && STAGES > 2;
+  auto slot = [&](const TileC& t, int s) -> char* {
+    if constexpr (EARLY) return smem + ((t.base + s) % STAGES) * SBYTES;
+    else return smem + (s % STAGES) * SBYTES;
   };
   int ehint = 0;                   // group of the previous tile of this block
   auto setup = [&](int Lt) {
     TileC t;
-    t.e = find_group_from(p.tprefix, p.tscale, p.groups, Lt, ehint);
+    t.base = 0;
+    t.e = find_group_plan(p.tprefix, p.tscale, p.groups, Lt, ehint);
     ehint = t.e;
-    const int q = Lt - p.tprefix[t.e] * p.tscale;
-    t.off = p.offsets[t.e];
-    const int cnt = p.offsets[t.e + 1] - t.off;
+    const int q = Lt - ld_plan(p.tprefix, t.e) * p.tscale;
+    t.off = ld_plan(p.offsets, t.e);
+    const int cnt = ld_plan(p.offsets, t.e + 1) - t.off;
     if constexpr (GM == GROUP_M) {
       const int mt_e = (cnt + BM - 1) / BM;
       t.m0 = (q % mt_e) * BM; t.n0 = (q / mt_e) * BN;
@@ -251,7 +301,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
     return t;
   };
   auto issue = [&](const TileC& t, int kt) {
-    char* buf = smem + (kt % STAGES) * SBYTES;
+    char* buf = slot(t, kt);
     const int k0 = kt * BK;
     if constexpr (A_T) TA::load(t.Ab + (int64_t)k0 * p.lda, p.lda, t.mvalid, t.kvalid - k0, buf, wave, lane);
     else TA::load(t.Ab + k0, p.lda, t.mvalid, buf, wave, lane);
@@ -270,7 +320,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
     if constexpr (GM == GROUP_K) {
       const int kv = t.kvalid - s * BK;
       if (kv < BK) {
-        char* buf = smem + (s % STAGES) * SBYTES;
+        char* buf = slot(t, s);
         block_sync_lds();
         TA::zero_tail(buf, kv, tid, NT);
         TB::zero_tail(buf + ABYTES, kv, tid, NT);
@@ -288,6 +338,8 @@ grouped_gemm2(GemmArgs<bf16> p) {
     const TileC t = nxt;
     const int e = t.e, off = t.off, m0 = t.m0, n0 = t.n0, mvalid = t.mvalid, nvalid = t.nvalid;
     const int nk = t.nk;
+    const bool more = L + Lstep < Lend;
+    int early = 0;                 // stages of the next tile issued before this tile's MFMAs
     const int nblk = (mvalid + 31) / 32;                 // live 32-row blocks of the tile
     int nl = (nblk - wm + WM - 1) / WM;                  // of them, this wave's (a prefix of j)
     nl = nl < 0 ? 0 : (nl > TM ? TM : nl);
@@ -341,11 +393,22 @@ grouped_gemm2(GemmArgs<bf16> p) {
         wait_stage(issued - 1, prev_stores);
         fix_tail(t, 0);
         block_sync_lds();
-        ldfrag(smem, 0, 0);
+        ldfrag(slot(t, 0), 0, 0);
+      }
+      if constexpr (EARLY) {
+        // every stage of this tile is already issued and the slots past its last one
+        // held the previous tile's stages, consumed before the previous tile's final
+        // barrier: fill them with the next tile's first stages
+        if (more && nk < STAGES) {
+          nxt = setup(L + Lstep);
+          nxt.base = (t.base + nk) % STAGES;
+          early = nxt.nk < STAGES - nk ? nxt.nk : STAGES - nk;
+          for (int st = 0; st < early; ++st) issue(nxt, st);
+        }
       }
       // every stage but the last: the last MFMA step also moves on to the next stage
       for (int kt = 0; kt + 1 < nk; ++kt) {
-        const char* cur = smem + (kt % STAGES) * SBYTES;
+        const char* cur = slot(t, kt);
 #pragma unroll
         for (int kk = 0; kk + 1 < KK; ++kk) {
           ldfrag(cur, kk + 1, (kk & 1) ^ 1);
@@ -361,17 +424,18 @@ grouped_gemm2(GemmArgs<bf16> p) {
           // stages issued after kt+1: up to kt+STAGES-1, capped by the last stage; the
           // previous epilogue's stores come after the prologue stages 0..STAGES-1
           const int last = kt + STAGES - 1 < nk - 1 ? kt + STAGES - 1 : nk - 1;
-          wait_stage(last - (kt + 1), kt + 1 < STAGES ? prev_stores : 0);
+          // (the next tile's early stages were issued after all of this tile's)
+          wait_stage(last - (kt + 1), (kt + 1 < STAGES ? prev_stores : 0) + early * LPS);
         }
         fix_tail(t, kt + 1);
         block_sync_lds();               // every wave is done with slot kt and sees stage kt+1
         if (kt + STAGES < nk) issue(t, kt + STAGES);
-        ldfrag(smem + ((kt + 1) % STAGES) * SBYTES, 0, 0);
+        ldfrag(slot(t, kt + 1), 0, 0);
         mm(1);
         interleave();
       }
       {
-        const char* cur = smem + ((nk - 1) % STAGES) * SBYTES;
+        const char* cur = slot(t, nk - 1);
 #pragma unroll
         for (int kk = 0; kk + 1 < KK; ++kk) {
           ldfrag(cur, kk + 1, (kk & 1) ^ 1);
@@ -411,11 +475,13 @@ grouped_gemm2(GemmArgs<bf16> p) {
         }
     }
 
-    const bool more = L + Lstep < Lend;
     if (more) {
-      nxt = setup(L + Lstep);
+      if (early == 0) {
+        nxt = setup(L + Lstep);
+        if constexpr (EARLY) nxt.base = (t.base + nk) % STAGES;
+      }
 #pragma unroll
-      for (int st = 0; st < PRE; ++st)
+      for (int st = early; st < PRE; ++st)
         if (st < nxt.nk) issue(nxt, st);
     }
 
@@ -528,7 +594,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
       prev_stores = 0;
       if (more) {
 #pragma unroll
-        for (int st = PRE; st < STAGES; ++st)
+        for (int st = PRE > early ? PRE : early; st < STAGES; ++st)
           if (st < nxt.nk) issue(nxt, st);
       }
     }
