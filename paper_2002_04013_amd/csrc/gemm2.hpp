@@ -24,32 +24,23 @@
 namespace dmoe {
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
-typedef __attribute__((address_space(1))) void* glb_ptr_t;
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ void g2l_16(const void* g, void* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds((glb_ptr_t)g, (lds_ptr_t)lds_wave_base, 16, 0, 0);
-}
-// The same from a wave-uniform base and a 32-bit per-lane byte offset: one address
-// register per load instead of a 64-bit pointer (the scalar-base addressing form).
+// Direct global->LDS load of 16 bytes per lane into the wave's 1 KiB at lds_wave_base,
+// from a wave-uniform base and a 32-bit per-lane byte offset (the scalar-base form: one
+// address register per load).  Written out as the instruction (M0 = the wave's LDS
+// destination, one wait state before the load reads it) rather than through the
+// compiler builtin, so the compiler does not track it and adds no waits of its own:
+//   * it cannot tell the LDS operand of a transposing read (ds_read_b64_tr_b16) apart
+//     from these loads' destinations and would drain every outstanding load
+//     (vmcnt(0)) before each such read, serialising the ring;
+//   * its waits for the epilogue's own loads (bias, h, old parameters) then count only
+//     those loads; in-order retirement makes them cover the ring loads issued before.
+// The pipeline's counted vmcnt waits and barriers order these loads.
 __device__ __forceinline__ void g2l_16_at(const bf16* base, uint32_t off_bytes, void* lds_wave_base) {
-  g2l_16(reinterpret_cast<const char*>(base) + off_bytes, lds_wave_base);
-}
-// The same load written out as the instruction (M0 = the wave's LDS destination, one
-// wait state before the load reads it).  The compiler does not know it writes LDS, so
-// it adds no wait of its own for it: it would otherwise drain every outstanding
-// direct-to-LDS load (vmcnt(0)) before each transposing LDS read (ds_read_b64_tr_b16),
-// whose LDS operand it cannot tell apart from the loads' destinations, serialising
-// the ring.  The pipeline's own vmcnt waits and barriers order these loads.
-__device__ __forceinline__ void g2l_16_at_asm(const bf16* base, uint32_t off_bytes, void* lds_wave_base) {
   const uint32_t m = (uint32_t)(uintptr_t)(lds_ptr_t)lds_wave_base;
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                :: "v"(off_bytes), "s"(base), "s"(m) : "memory", "m0");
-}
-template <bool ASM>
-__device__ __forceinline__ void g2l_tile(const bf16* base, uint32_t off_bytes, void* lds_wave_base) {
-  if constexpr (ASM) g2l_16_at_asm(base, off_bytes, lds_wave_base);
-  else g2l_16_at(base, off_bytes, lds_wave_base);
 }
 
 // s_waitcnt vmcnt(n) with expcnt/lgkmcnt left free (gfx9 encoding).
@@ -77,7 +68,7 @@ __device__ __forceinline__ int swz_kc(int r) {
 }
 
 // ---- K-contiguous tile [R][BK] -------------------------------------------------------
-template <int R, int NW, int SW, int BK, bool ASM = false>
+template <int R, int NW, int SW, int BK>
 struct KcTile {
   static constexpr int RB = BK * 2;                    // bytes per row
   static constexpr int CH = BK / 8;                    // chunks per row
@@ -97,7 +88,7 @@ struct KcTile {
       const int r = q * RPI + lane / CH;
       const int c = (lane % CH) ^ swz_kc<BK, SW>(r);
       const int rr = r < rvalid ? r : rvalid - 1;
-      g2l_tile<ASM>(base, ((uint32_t)rr * (uint32_t)ld + (uint32_t)(c * 8)) * 2u, lds + q * 1024);
+      g2l_16_at(base, ((uint32_t)rr * (uint32_t)ld + (uint32_t)(c * 8)) * 2u, lds + q * 1024);
     }
   }
   // fragment of rows r0 + (lane % 32), k chunk kc + lane / 32 (8 bf16)
@@ -109,7 +100,7 @@ struct KcTile {
 };
 
 // ---- N-contiguous tile [BK][R] (row = k) ---------------------------------------------
-template <int R, int NW, int BK, bool ASM = false>
+template <int R, int NW, int BK>
 struct NcTile {
   static constexpr int BYTES = BK * R * 2;
   static constexpr int CPR = R / 8;                    // chunks per row
@@ -131,7 +122,7 @@ struct NcTile {
       int col = c * 8;
       col = col < cvalid ? col : ((cvalid - 1) & ~7);
       const int kk = k < kvalid ? k : kvalid - 1;
-      g2l_tile<ASM>(base, ((uint32_t)kk * (uint32_t)ld + (uint32_t)col) * 2u, lds + q * 1024);
+      g2l_16_at(base, ((uint32_t)kk * (uint32_t)ld + (uint32_t)col) * 2u, lds + q * 1024);
     }
   }
   // zero rows [kvalid, BK) of the tile (GROUP_K tail)
@@ -217,11 +208,8 @@ grouped_gemm2(GemmArgs<bf16> p) {
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int KK = BK / 16;
-  // kernels with transposing LDS reads issue their direct-to-LDS loads as written-out
-  // instructions (see g2l_16_at_asm)
-  constexpr bool DMA_ASM = A_T || B_T;
-  using TA = typename std::conditional<A_T, NcTile<BM, NW, BK, DMA_ASM>, KcTile<BM, NW, SW, BK, DMA_ASM>>::type;
-  using TB = typename std::conditional<B_T, NcTile<BN, NW, BK, DMA_ASM>, KcTile<BN, NW, SW, BK, DMA_ASM>>::type;
+  using TA = typename std::conditional<A_T, NcTile<BM, NW, BK>, KcTile<BM, NW, SW, BK>>::type;
+  using TB = typename std::conditional<B_T, NcTile<BN, NW, BK>, KcTile<BN, NW, SW, BK>>::type;
   constexpr int ABYTES = TA::BYTES, SBYTES = TA::BYTES + TB::BYTES;
   constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave
   // store instructions of a full tile's epilogue, per wave
