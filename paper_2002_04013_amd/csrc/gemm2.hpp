@@ -37,10 +37,22 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 //   * its waits for the epilogue's own loads (bias, h, old parameters) then count only
 //     those loads; in-order retirement makes them cover the ring loads issued before.
 // The pipeline's counted vmcnt waits and barriers order these loads.
-__device__ __forceinline__ void g2l_16_at(const bf16* base, uint32_t off_bytes, void* lds_wave_base) {
-  const uint32_t m = (uint32_t)(uintptr_t)(lds_ptr_t)lds_wave_base;
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :: "v"(off_bytes), "s"(base), "s"(m) : "memory", "m0");
+// The LDS destination is lds_base + LOFF, LOFF a compile-time byte offset, so one
+// scalar register serves every load of a stage.
+template <int LOFF>
+__device__ __forceinline__ void g2l_16_at(const bf16* base, uint32_t off_bytes, char* lds_base) {
+  const uint32_t m = (uint32_t)(uintptr_t)(lds_ptr_t)lds_base;
+  asm volatile("s_add_u32 m0, %2, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off_bytes), "s"(base), "s"(m), "i"(LOFF) : "memory", "m0");
+}
+
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N-1>), in order
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
 }
 
 // s_waitcnt vmcnt(n) with expcnt/lgkmcnt left free (gfx9 encoding).
@@ -81,15 +93,16 @@ struct KcTile {
   // issue this wave's loads: rows [0, R) of the tile starting at `base` (row stride ld)
   __device__ __forceinline__ static void load(const bf16* base, int64_t ld, int rvalid, char* lds, int wave,
                                               int lane) {
-#pragma unroll
-    for (int i = 0; i < PER_WAVE; ++i) {
+    char* lw = lds + wave * 1024;
+    static_for<PER_WAVE>([&](auto I) {
+      constexpr int i = decltype(I)::value;
       const int q = wave + i * NW;
-      if (INSTR % NW != 0 && q >= INSTR) break;
+      if (INSTR % NW != 0 && q >= INSTR) return;
       const int r = q * RPI + lane / CH;
       const int c = (lane % CH) ^ swz_kc<BK, SW>(r);
       const int rr = r < rvalid ? r : rvalid - 1;
-      g2l_16_at(base, ((uint32_t)rr * (uint32_t)ld + (uint32_t)(c * 8)) * 2u, lds + q * 1024);
-    }
+      g2l_16_at<i * NW * 1024>(base, ((uint32_t)rr * (uint32_t)ld + (uint32_t)(c * 8)) * 2u, lw);
+    });
   }
   // fragment of rows r0 + (lane % 32), k chunk kc + lane / 32 (8 bf16)
   __device__ __forceinline__ static bf16x8_t frag(const char* lds, int r0, int kc, int lane) {
@@ -112,18 +125,19 @@ struct NcTile {
   // element (col c, k) at base[k * ld + c]; rows k >= kvalid clamped (zeroed later)
   __device__ __forceinline__ static void load(const bf16* base, int64_t ld, int cvalid, int kvalid, char* lds,
                                               int wave, int lane) {
-#pragma unroll
-    for (int i = 0; i < PER_WAVE; ++i) {
+    char* lw = lds + wave * 1024;
+    static_for<PER_WAVE>([&](auto I) {
+      constexpr int i = decltype(I)::value;
       const int q = wave + i * NW;
-      if (INSTR % NW != 0 && q >= INSTR) break;
+      if (INSTR % NW != 0 && q >= INSTR) return;
       const int k = q * RPI + lane / CPR;
       const int pos = lane % CPR;
       const int c = pos ^ swz(k);
       int col = c * 8;
       col = col < cvalid ? col : ((cvalid - 1) & ~7);
       const int kk = k < kvalid ? k : kvalid - 1;
-      g2l_16_at(base, ((uint32_t)kk * (uint32_t)ld + (uint32_t)col) * 2u, lds + q * 1024);
-    }
+      g2l_16_at<i * NW * 1024>(base, ((uint32_t)kk * (uint32_t)ld + (uint32_t)col) * 2u, lw);
+    });
   }
   // zero rows [kvalid, BK) of the tile (GROUP_K tail)
   __device__ __forceinline__ static void zero_tail(char* lds, int kvalid, int tid, int nt) {
