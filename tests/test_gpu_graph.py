@@ -83,3 +83,69 @@ def test_graph_replay_matches_eager(name):
         for n, v in eager.items():
             assert torch.equal(got[n], v), f"replay {r}: {n} differs from the eager step"
         say(f"[graph] {name}: replay {r} matches")
+
+
+BLOCK_CASES = {
+    # LayerNorm block experts, few rows per expert (32-row tiles) and many (256x256 tiles)
+    "block_bf16_skinny": Workload("graph_block_skinny", 42, T=300, D=128, H=256, d=2, M=4, k=2, dtype="bf16",
+                                  act="relu", p_alive=0.9, expert="ffblock"),
+    "block_bf16_fat": Workload("graph_block_fat", 43, T=1600, D=128, H=256, d=2, M=3, k=2, dtype="bf16",
+                               act="gelu", expert="ffblock"),
+}
+
+
+@pytest.mark.parametrize("name", list(BLOCK_CASES))
+def test_block_graph_replay_matches_eager(name):
+    """The same for the layer with LayerNorm block experts (gate, dispatch, the block's
+    grouped GEMMs and LayerNorm row kernels, combine, and their backward)."""
+    from paper_2002_04013_amd import DMoEBlockLayer
+    from workloads import make_block_inputs
+    wl = BLOCK_CASES[name]
+    say(f"[graph] {name}: T={wl.T} D={wl.D} F={wl.H} d={wl.d} M={wl.M} k={wl.k} {wl.dtype} {wl.act}")
+    dev = torch.device("cuda")
+    inp = make_block_inputs(wl, "cpu")
+    t = {n: v.to(dev) for n, v in inp.items() if n != "params"}
+    prm = {n: v.to(dev) for n, v in inp["params"].items()}
+    L = DMoEBlockLayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev)
+    grads = {n: torch.empty_like(v) for n, v in prm.items()}
+    dWg, dbg = torch.empty_like(t["Wg"]), torch.empty_like(t["bg"])
+
+    def step():
+        L.forward(t["x"], t["Wg"], t["bg"], t["alive"], prm)
+        L.backward(t["dy"], t["x"], t["Wg"], t["alive"], prm, grads, dWg, dbg)
+
+    def results():
+        out = {n: getattr(L, n) for n in ("idx", "w", "counts", "offsets", "y", "dw", "dg", "dx")}
+        out.update({"g_" + n: v for n, v in grads.items()}, dWg=dWg, dbg=dbg)
+        return {n: v.clone() for n, v in out.items()}
+
+    def reset_grads():
+        for v in grads.values():
+            v.fill_(7.0)
+
+    reset_grads()
+    step()
+    torch.cuda.synchronize()
+    eager = results()
+    say(f"[graph] {name}: eager step done")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    for r in range(REPLAYS):
+        for n in ("y", "dx", "w", "dw", "dg"):
+            getattr(L, n).fill_(float("nan"))
+        for v in L.acts.values():
+            v.fill_(float("nan"))
+        L.idx.fill_(-5)
+        L.ws.fill_(0x5A if r % 2 == 0 else 0xC3)
+        dWg.fill_(-1.0)
+        dbg.fill_(-1.0)
+        reset_grads()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = results()
+        for n, v in eager.items():
+            assert torch.equal(got[n], v), f"replay {r}: {n} differs from the eager step"
+        say(f"[graph] {name}: replay {r} matches")
