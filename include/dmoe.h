@@ -87,6 +87,24 @@ size_t dmoe_workspace_bytes(const dmoe_dims* dims);
 /* Static text for a return code. */
 const char* dmoe_strerror(int code);
 
+/* Launch trace, a measurement aid (it implements no part of the layer).  After
+ * dmoe_trace_begin(events, names, capacity) on a host thread, each kernel that an entry
+ * point called from that thread enqueues is followed, on the same stream, by
+ * hipEventRecord(events[i]) for the i-th such kernel (i < capacity; later ones are
+ * counted but not recorded), and names[i] is set to a static string naming the kernel.
+ *   events  [capacity]  hipEvent_t handles (as void*), created and owned by the caller
+ *   names   [capacity]  host array the library fills
+ * The device time of kernel i is the time from events[i-1] (for i = 0: an event the
+ * caller records on the stream before its first traced call) to events[i]; on one
+ * stream kernels run in order, so these intervals partition the traced calls.
+ * dmoe_trace_end() stops the trace and returns the number of kernels enqueued while
+ * it was active (which may exceed capacity).  Without an active trace nothing is
+ * recorded.  The trace state is per host thread; it is the caller's job not to combine
+ * a trace with HIP graph capture.  Returns DMOE_EINVAL for capacity < 0 or, with
+ * capacity > 0, NULL arrays. */
+int dmoe_trace_begin(void* const* events, const char** names, int capacity);
+int dmoe_trace_end(void);
+
 /* Gate scores, exact TopK over the grid and Eq. 1 weights (Sec. 3.2; Eq. 1; App. C).
  *   x      [T, D]      layer input
  *   Wg     [d*M, D]    rows i*M .. i*M+M-1 are the weight of g_i (nn.Linear layout)

@@ -24,6 +24,7 @@ EXPORTS = (
     "dmoe_expert_ffn_fwd", "dmoe_combine", "dmoe_combine_bwd", "dmoe_gate_topk_bwd",
     "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd", "dmoe_expert_ffn_bwd_recompute", "dmoe_expert_ffn_bwd_sgd",
     "dmoe_expert_ffblock_fwd", "dmoe_expert_ffblock_bwd", "dmoe_ln_act_fwd", "dmoe_ln_act_bwd",
+    "dmoe_trace_begin", "dmoe_trace_end",
 )
 
 # parameters of the feed-forward block expert, in dmoe_ffblock_params order
@@ -88,6 +89,9 @@ def load(path=LIB_PATH):
                                                    ctypes.POINTER(FFBlockParams), _P, _P]),
         "dmoe_ln_act_fwd": (ctypes.c_int, [pd] + [_P] * 7),
         "dmoe_ln_act_bwd": (ctypes.c_int, [pd] + [_P] * 10),
+        "dmoe_trace_begin": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_char_p),
+                                            ctypes.c_int]),
+        "dmoe_trace_end": (ctypes.c_int, []),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -226,3 +230,34 @@ def dmoe_ln_act_bwd(dims, offsets, h, stats, gamma, beta, da, dh, dgamma, dbeta,
     _check(load().dmoe_ln_act_bwd(ctypes.byref(dims), _ptr(offsets), _ptr(h), _ptr(stats), _ptr(gamma),
                                   _ptr(beta), _ptr(da), _ptr(dh), _ptr(dgamma), _ptr(dbeta), _stream(stream)),
            "dmoe_ln_act_bwd")
+
+
+class Trace:
+    """Launch trace of the library (dmoe_trace_begin / dmoe_trace_end): every kernel the
+    calls made inside the `with` block enqueue is followed by a record of the next of
+    `capacity` timing events on its stream.  After the block, `kernels()` gives
+    (name, milliseconds) per traced kernel once the stream has reached them."""
+
+    def __init__(self, capacity=256, stream=None):
+        self.stream = torch.cuda.current_stream() if stream is None else stream
+        self.events = [torch.cuda.Event(enable_timing=True) for _ in range(capacity + 1)]
+        for e in self.events:          # torch creates the HIP event on its first record
+            e.record(self.stream)
+        self._handles = (ctypes.c_void_p * capacity)(*[e.cuda_event for e in self.events[1:]])
+        self._names = (ctypes.c_char_p * capacity)()
+        self.capacity = capacity
+        self.count = 0
+
+    def __enter__(self):
+        self.events[0].record(self.stream)
+        _check(load().dmoe_trace_begin(self._handles, self._names, self.capacity), "dmoe_trace_begin")
+        return self
+
+    def __exit__(self, *exc):
+        self.count = int(load().dmoe_trace_end())
+        return False
+
+    def kernels(self):
+        self.events[-1].synchronize()
+        n = min(self.count, self.capacity)
+        return [(self._names[i].decode(), self.events[i].elapsed_time(self.events[i + 1])) for i in range(n)]

@@ -76,13 +76,30 @@ __global__ void fill_zero_kernel(unsigned char* p, size_t bytes) {
 void fill_zero(void* p, size_t bytes, hipStream_t st) {
   if (!bytes) return;
   const size_t blocks = std::min<size_t>((bytes + 255) / 256, 1024);
-  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+  DMOE_LAUNCH(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
                      reinterpret_cast<unsigned char*>(p), bytes);
 }
+
+thread_local TraceState* t_trace = nullptr;
+static thread_local TraceState t_trace_state;
 
 }  // namespace dmoe
 
 using namespace dmoe;
+
+extern "C" int dmoe_trace_begin(void* const* events, const char** names, int capacity) {
+  if (capacity < 0 || (capacity > 0 && (!events || !names))) return DMOE_EINVAL;
+  t_trace_state = TraceState{events, names, capacity, 0};
+  t_trace = &t_trace_state;
+  return DMOE_OK;
+}
+
+extern "C" int dmoe_trace_end(void) {
+  if (!t_trace) return 0;
+  const int n = t_trace->n;
+  t_trace = nullptr;
+  return n;
+}
 
 extern "C" size_t dmoe_workspace_bytes(const dmoe_dims* dims) {
   Shape s;

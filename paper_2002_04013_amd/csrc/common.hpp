@@ -135,6 +135,33 @@ struct Shape {
 
 int check_dims(const dmoe_dims* dims, Shape* s);
 
+// Launch trace (dmoe_trace_begin / dmoe_trace_end): while a trace is active on the
+// calling host thread, every kernel an entry point enqueues is followed on its stream by
+// a record of the caller's next event, and the kernel's name is noted beside it.
+struct TraceState {
+  void* const* events;   // hipEvent_t handles, caller-owned
+  const char** names;
+  int cap, n;
+};
+extern thread_local TraceState* t_trace;
+inline void trace_mark(hipStream_t st, const char* name) {
+  TraceState* t = t_trace;
+  if (!t) return;
+  if (t->n < t->cap) {
+    (void)hipEventRecord(reinterpret_cast<hipEvent_t>(t->events[t->n]), st);
+    t->names[t->n] = name;
+  }
+  ++t->n;
+}
+// Every kernel of the library is enqueued through these: a launch, then its trace mark.
+#define DMOE_LAUNCH_NAMED(name, kernel, grid, block, lds, st, ...)          \
+  do {                                                                     \
+    hipLaunchKernelGGL(kernel, grid, block, lds, st, __VA_ARGS__);         \
+    ::dmoe::trace_mark(st, name);                                          \
+  } while (0)
+#define DMOE_LAUNCH(kernel, grid, block, lds, st, ...) \
+  DMOE_LAUNCH_NAMED(#kernel, kernel, grid, block, lds, st, __VA_ARGS__)
+
 inline int launch_status() {
   return hipGetLastError() == hipSuccess ? DMOE_OK : DMOE_EHIP;
 }

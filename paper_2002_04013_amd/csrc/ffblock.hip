@@ -282,10 +282,10 @@ static void ln_fwd_act(const Shape& s, const int32_t* offsets, const E* h, const
                        float* stats, hipStream_t st) {
   const int N = (int)s.N, F = (int)s.H, grid = ln_grid(s);
   switch (ln_chunks<E>(F)) {
-    case 1: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 1, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
-    case 2: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 2, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
-    case 4: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 4, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
-    default: hipLaunchKernelGGL((ln_act_fwd_kernel<E, 8, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
+    case 1: DMOE_LAUNCH((ln_act_fwd_kernel<E, 1, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
+    case 2: DMOE_LAUNCH((ln_act_fwd_kernel<E, 2, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
+    case 4: DMOE_LAUNCH((ln_act_fwd_kernel<E, 4, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
+    default: DMOE_LAUNCH((ln_act_fwd_kernel<E, 8, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, offsets, N, F, g, b, a, stats); break;
   }
 }
 template <typename E>
@@ -301,13 +301,13 @@ static void ln_bwd_act(const Shape& s, const int32_t* offsets, const E* h, const
                        const E* b, const E* da, E* dh, E* dg, E* db, hipStream_t st) {
   const int N = (int)s.N, F = (int)s.H, grid = ln_grid(s);
   constexpr int VEC = Vec<E>::N;
-  hipLaunchKernelGGL((ln_act_bwd_params_kernel<E, ACT>), dim3((unsigned)((F / VEC + 255) / 256), (unsigned)N),
+  DMOE_LAUNCH((ln_act_bwd_params_kernel<E, ACT>), dim3((unsigned)((F / VEC + 255) / 256), (unsigned)N),
                      dim3(256), 0, st, h, stats, offsets, F, g, b, da, dg, db);
   switch (ln_chunks<E>(F)) {
-    case 1: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 1, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
-    case 2: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 2, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
-    case 4: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 4, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
-    default: hipLaunchKernelGGL((ln_act_bwd_rows_kernel<E, 8, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
+    case 1: DMOE_LAUNCH((ln_act_bwd_rows_kernel<E, 1, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
+    case 2: DMOE_LAUNCH((ln_act_bwd_rows_kernel<E, 2, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
+    case 4: DMOE_LAUNCH((ln_act_bwd_rows_kernel<E, 4, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
+    default: DMOE_LAUNCH((ln_act_bwd_rows_kernel<E, 8, ACT>), dim3(grid), dim3(LN_NT), 0, st, h, stats, offsets, N, F, g, b, da, dh); break;
   }
 }
 template <typename E>
@@ -367,7 +367,7 @@ static void lin_wgrad(const Shape& s, const int32_t* offsets, const int32_t* tac
   p.C = dW; p.ldc = n_in; p.c_gstride = (int64_t)n_out * n_in;
   p.M = n_out; p.N = n_in; p.act = s.act;
   if constexpr (sizeof(E) == 2)
-    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
+    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK, CW::STO>(p, active_ub * mt * nt, st);
   else
     run_gemm<E, GROUP_K, false, EPI_STORE, CW::BM, CW::BN, CW::BK, CW::WM, CW::WN>(p, active_ub * mt * nt, st);
 }
@@ -375,7 +375,7 @@ static void lin_wgrad(const Shape& s, const int32_t* offsets, const int32_t* tac
 template <typename E>
 static void colsum(const Shape& s, const int32_t* offsets, const E* X, int ncols, E* out, hipStream_t st) {
   constexpr int VEC = Vec<E>::N;
-  hipLaunchKernelGGL((segment_colsum<E>), dim3((unsigned)((ncols / VEC + 255) / 256), (unsigned)s.N), dim3(256), 0,
+  DMOE_LAUNCH((segment_colsum<E>), dim3((unsigned)((ncols / VEC + 255) / 256), (unsigned)s.N), dim3(256), 0,
                      st, X, (int64_t)ncols, offsets, ncols, out, 0.f);
 }
 
@@ -394,7 +394,7 @@ template <typename E, typename C>
 static void block_fwd(const Shape& s, const int32_t* offsets, const E* xp, const BlockP<E>& q, const BlockA<E>& t,
                       E* yp, int32_t* tpre, hipStream_t st) {
   const int D = (int)s.D, F = (int)s.H;
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, (int)s.N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, (int)s.N, C::BM, tpre);
   lin_fwd<E, C>(s, offsets, tpre, xp, D, q.W1, q.b1, F, t.h1, st);
   ln_fwd<E>(s, offsets, t.h1, q.g1, q.be1, t.a1, t.st1, st);
   lin_fwd<E, C>(s, offsets, tpre, t.a1, F, q.W2, q.b2, F, t.h2, st);
@@ -408,7 +408,7 @@ static void block_bwd(const Shape& s, const int32_t* offsets, const E* xp, const
                       const E* dyp, E* g1, E* g2, E* dxp, const BlockG<E>& d, int32_t* tpre, hipStream_t st) {
   const int D = (int)s.D, F = (int)s.H;
   const int32_t* tact = tpre + s.N + 1;
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, (int)s.N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, (int)s.N, C::BM, tpre);
   lin_wgrad<E, CW>(s, offsets, tact, dyp, D, t.a2, F, d.W3, st);     // dW3 = dy^T a2
   colsum<E>(s, offsets, dyp, D, d.b3, st);                            // db3
   lin_dgrad<E, C>(s, offsets, tpre, dyp, D, q.W3, F, g2, st);        // da2 = dy W3

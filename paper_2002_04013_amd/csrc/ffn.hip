@@ -12,7 +12,7 @@ static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
                          int32_t* tpre, hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   {
     const int nt = (H + C::BN - 1) / C::BN;
     GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
@@ -42,7 +42,7 @@ static void ffn_up_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, 
                         bf16* h, bf16* a, int32_t* tpre, hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   const int nt = (H + C::BN - 1) / C::BN;
   GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
   p.A = xp; p.lda = D;
@@ -61,7 +61,7 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
   const int64_t active_ub = std::min<int64_t>(s.N, s.P);
   const int32_t* tact = tpre + N + 1;
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   {   // dh = (dy W2) * act'(h): W2_e read as (n = h, k = d), N-contiguous
     const int nt = (H + C::BN - 1) / C::BN;
     GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
@@ -78,7 +78,7 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.B = a; p.ldb = H;
     p.C = dW2; p.ldc = H; p.c_gstride = (int64_t)D * H;
     p.M = D; p.N = H; p.act = s.act;
-    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
+    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK, CW::STO>(p, active_ub * mt * nt, st);
   }
   {   // dx_perm = dh W1: W1_e read as (n = d, k = h), N-contiguous
     const int nt = (D + C::BN - 1) / C::BN;
@@ -96,11 +96,11 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.B = xp; p.ldb = D;
     p.C = dW1; p.ldc = D; p.c_gstride = (int64_t)H * D;
     p.M = H; p.N = D; p.act = s.act;
-    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
+    run_gemm2<GROUP_K, true, true, EPI_STORE, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK, CW::STO>(p, active_ub * mt * nt, st);
   }
-  hipLaunchKernelGGL(segment_colsum<bf16>, dim3((unsigned)((H / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
+  DMOE_LAUNCH(segment_colsum<bf16>, dim3((unsigned)((H / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
                      st, dh, (int64_t)H, offsets, H, db1);
-  hipLaunchKernelGGL(segment_colsum<bf16>, dim3((unsigned)((D / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
+  DMOE_LAUNCH(segment_colsum<bf16>, dim3((unsigned)((D / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
                      st, dyp, (int64_t)D, offsets, D, db2);
 }
 
@@ -115,7 +115,7 @@ static void ffn_bwd_sgd_bf16(const Shape& s, const int32_t* offsets, const bf16*
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
   const int64_t active_ub = std::min<int64_t>(s.N, s.P);
   const int32_t* tact = tpre + N + 1;
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   {   // dh = (dy W2) * act'(h)
     const int nt = (H + C::BN - 1) / C::BN;
     GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
@@ -132,7 +132,7 @@ static void ffn_bwd_sgd_bf16(const Shape& s, const int32_t* offsets, const bf16*
     p.B = a; p.ldb = H;
     p.C = W2; p.ldc = H; p.c_gstride = (int64_t)D * H;
     p.M = D; p.N = H; p.act = s.act; p.lr = lr;
-    run_gemm2<GROUP_K, true, true, EPI_SGD, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
+    run_gemm2<GROUP_K, true, true, EPI_SGD, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK, CW::STO>(p, active_ub * mt * nt, st);
   }
   {   // dx_perm = dh W1
     const int nt = (D + C::BN - 1) / C::BN;
@@ -150,11 +150,11 @@ static void ffn_bwd_sgd_bf16(const Shape& s, const int32_t* offsets, const bf16*
     p.B = xp; p.ldb = D;
     p.C = W1; p.ldc = D; p.c_gstride = (int64_t)H * D;
     p.M = H; p.N = D; p.act = s.act; p.lr = lr;
-    run_gemm2<GROUP_K, true, true, EPI_SGD, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK>(p, active_ub * mt * nt, st);
+    run_gemm2<GROUP_K, true, true, EPI_SGD, CW::BM, CW::BN, CW::WM, CW::WN, CW::ST, CW::BK, CW::STO>(p, active_ub * mt * nt, st);
   }
-  hipLaunchKernelGGL((segment_colsum<bf16, true>), dim3((unsigned)((H / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
+  DMOE_LAUNCH((segment_colsum<bf16, true>), dim3((unsigned)((H / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
                      st, dh, (int64_t)H, offsets, H, b1, lr);
-  hipLaunchKernelGGL((segment_colsum<bf16, true>), dim3((unsigned)((D / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
+  DMOE_LAUNCH((segment_colsum<bf16, true>), dim3((unsigned)((D / 8 + 255) / 256), (unsigned)N), dim3(256), 0,
                      st, dyp, (int64_t)D, offsets, D, b2, lr);
 }
 
@@ -164,7 +164,7 @@ static void ffn_fwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
                         hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   // h = x W1^T + b1, a = act(h)
   {
     const int nt = (H + C::BN - 1) / C::BN;
@@ -201,7 +201,7 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
   const int64_t active_ub = std::min<int64_t>(s.N, s.P);
   const int32_t* tact = tpre + N + 1;
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   // dh = (dy W2) * act'(h)       B = W2_e viewed as (n = h, k = d): N-contiguous
   {
     const int nt = (H + C::BN - 1) / C::BN;
@@ -244,9 +244,9 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
   }
   // bias gradients
   constexpr int VEC = 16 / sizeof(E);
-  hipLaunchKernelGGL((segment_colsum<E, SGD>), dim3((unsigned)((H / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
+  DMOE_LAUNCH((segment_colsum<E, SGD>), dim3((unsigned)((H / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
                      st, dh, (int64_t)H, offsets, H, db1, lr);
-  hipLaunchKernelGGL((segment_colsum<E, SGD>), dim3((unsigned)((D / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
+  DMOE_LAUNCH((segment_colsum<E, SGD>), dim3((unsigned)((D / VEC + 255) / 256), (unsigned)N), dim3(256), 0,
                      st, dyp, (int64_t)D, offsets, D, db2, lr);
 }
 
@@ -255,7 +255,7 @@ static void ffn_up_cfg(const Shape& s, const int32_t* offsets, const E* xp, cons
                        int32_t* tpre, hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
   const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
-  hipLaunchKernelGGL(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
   const int nt = (H + C::BN - 1) / C::BN;
   GemmArgs<E> p = args_m<E>(offsets, tpre, nt, N);
   p.A = xp; p.lda = D;

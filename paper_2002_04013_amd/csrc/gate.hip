@@ -927,12 +927,12 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
     if (!ws) return DMOE_EINVAL;
     if (!aligned16(ws)) return DMOE_EUNSUPPORTED;
     int32_t* queue = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + workspace_layout(s).gq_off);
-    hipLaunchKernelGGL(gate_queue_all, dim3((unsigned)((s.T + 255) / 256)), dim3(256), 0, st, queue, (int)s.T);
+    DMOE_LAUNCH(gate_queue_all, dim3((unsigned)((s.T + 255) / 256)), dim3(256), 0, st, queue, (int)s.T);
     const int xgrid = (int)std::min<int64_t>((s.T + GX_TB - 1) / GX_TB, 1024);
     if (s.dtype == DMOE_BF16)
-      hipLaunchKernelGGL((gate_exact_kernel<bf16, true>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+      DMOE_LAUNCH((gate_exact_kernel<bf16, true>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
     else
-      hipLaunchKernelGGL((gate_exact_kernel<float, true>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+      DMOE_LAUNCH((gate_exact_kernel<float, true>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
     return launch_status();
   }
   if (s.dtype == DMOE_BF16 && s.dM <= 3 * 32) {
@@ -955,21 +955,21 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
     }
     fill_zero(queue, sizeof(int32_t), st);
     const dim3 grid((unsigned)((s.T + GM_TOK - 1) / GM_TOK));
-    hipLaunchKernelGGL(kern, grid, dim3(64 * KW), lds, st, ga);
+    DMOE_LAUNCH_NAMED("gate_topk_mfma", kern, grid, dim3(64 * KW), lds, st, ga);
     // exact recomputation of the queued tokens: persistent blocks over the queue
     if (s.flags & DMOE_FLAG_GATE_EXACT) {
       const int xgrid = (int)std::min<int64_t>((s.T + GX_TB - 1) / GX_TB, 1024);
-      hipLaunchKernelGGL((gate_exact_kernel<bf16, false>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+      DMOE_LAUNCH((gate_exact_kernel<bf16, false>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
     } else {
       const int xgrid = (int)std::min<int64_t>(s.T, 1024);
-      hipLaunchKernelGGL(gate_exact_sparse_kernel, dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+      DMOE_LAUNCH(gate_exact_sparse_kernel, dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
     }
   } else {
     // fp32, and bf16 with more than 96 gate columns: exact fp64 scores for every token
     const dim3 grid((unsigned)((s.T + GATE_TB - 1) / GATE_TB));
     const size_t lds = gate_lds_bytes((int)s.dM);
-    if (s.dtype == DMOE_BF16) hipLaunchKernelGGL(gate_topk_kernel<bf16>, grid, dim3(GATE_NT), lds, st, a);
-    else hipLaunchKernelGGL(gate_topk_kernel<float>, grid, dim3(GATE_NT), lds, st, a);
+    if (s.dtype == DMOE_BF16) DMOE_LAUNCH(gate_topk_kernel<bf16>, grid, dim3(GATE_NT), lds, st, a);
+    else DMOE_LAUNCH(gate_topk_kernel<float>, grid, dim3(GATE_NT), lds, st, a);
   }
   return launch_status();
 }
@@ -994,13 +994,13 @@ static int gate_bwd_impl(const Shape& s, const void* x, const int32_t* idx, cons
     (void)hipFuncSetAttribute((const void*)gate_dg_kernel<E>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dg_lds);
     (void)hipGetLastError();
   }
-  hipLaunchKernelGGL(gate_dg_kernel<E>, dim3(gblk), dim3(GD_NT), dg_lds, st, idx, w, dw, alive, dg, ds, L.ds_ld, T,
+  DMOE_LAUNCH(gate_dg_kernel<E>, dim3(gblk), dim3(GD_NT), dg_lds, st, idx, w, dw, alive, dg, ds, L.ds_ld, T,
                      s.d, s.M, s.k, dM, dbg_part);
   // dWg partials: one GROUP_K GEMM group per token split, C[split] = ds_split^T x_split
   constexpr int BM = 64, BN = 128, BK = 32, WM = 2, WN = 2;
   const int rows = (int)L.ds_ld;                     // GEMM M (ds columns incl. lo part/padding)
   const int mt = (rows + BM - 1) / BM, nt = (D + BN - 1) / BN;
-  hipLaunchKernelGGL(gate_split_prep, dim3(1), dim3(256), 0, st, offs, tpre, (int)L.gsplit,
+  DMOE_LAUNCH(gate_split_prep, dim3(1), dim3(256), 0, st, offs, tpre, (int)L.gsplit,
                      (int)L.gsplit_tokens, T);
   GemmArgs<E> p{};
   p.A = ds; p.lda = L.ds_ld;
@@ -1013,12 +1013,13 @@ static int gate_bwd_impl(const Shape& s, const void* x, const int32_t* idx, cons
   const size_t lds = gemm_lds_bytes<E, BM, BN, BK, WM, WN>();
   int grid = tiles < 2048 ? tiles : 2048;
   p.chunked = grid >= 8;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * WM * WN), lds, st, p);
+  DMOE_LAUNCH_NAMED("grouped_gemm<GROUP_K,EPI_F32> (gate dWg per token split)", kern, dim3(grid),
+                    dim3(64 * WM * WN), lds, st, p);
   const int64_t outs = (int64_t)dM * D;
-  hipLaunchKernelGGL(gate_reduce_kernel<E>, dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, st,
+  DMOE_LAUNCH(gate_reduce_kernel<E>, dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, st,
                      part, (int)L.gsplit, (int64_t)rows, dM, D, reinterpret_cast<E*>(dWg));
   if (dbg)
-    hipLaunchKernelGGL(gate_dbg_kernel<E>, dim3(dM), dim3(256), 0, st, dbg_part, gblk, dM, reinterpret_cast<E*>(dbg));
+    DMOE_LAUNCH(gate_dbg_kernel<E>, dim3(dM), dim3(256), 0, st, dbg_part, gblk, dM, reinterpret_cast<E*>(dbg));
   return launch_status();
 }
 

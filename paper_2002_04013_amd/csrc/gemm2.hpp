@@ -198,6 +198,22 @@ __device__ __forceinline__ void wait_vmcnt_rt(int n) {
   else wait_vmcnt<0>();
 }
 
+// How the epilogue writes a bf16 output tile.
+//   STORE_DIRECT: each lane stores 16 contiguous bytes of its row straight from its
+//     registers (after a lane swap), so one wave instruction writes 32 rows x 32 bytes:
+//     every 128-byte line of the output is completed by four instructions.
+//   STORE_STAGED: each wave passes 32 rows x 64 columns of its output at a time through
+//     4 KiB of LDS of its own and stores whole lines: one wave instruction writes
+//     8 rows x 128 bytes.
+//   STORE_STAGED_NT: as STORE_STAGED, with the non-temporal hint on the stores.
+enum StoreMode { STORE_DIRECT = 0, STORE_STAGED = 1, STORE_STAGED_NT = 2 };
+constexpr int STG_WAVE_BYTES = 4096;
+
+// Staging layout of a wave's 32 x 64 piece: row r (0..31) holds 128 bytes, 16-byte
+// chunk c at position c ^ ((r / 2) % 8), so the 32 rows written at one chunk and the
+// 8 rows read per instruction spread over the LDS banks.
+__device__ __forceinline__ int stg_off(int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); }
+
 // Schedule of one tile, per wave:
 //   * the prologue issues every stage of the LDS ring (the ring is free once the
 //     previous tile's reads are done), before the previous tile's epilogue;
@@ -215,7 +231,8 @@ __device__ __forceinline__ void wait_vmcnt_rt(int n) {
 // as its block j = b / WM, so a partly filled tile (the last m-tile of an expert)
 // spreads its live blocks over all wave rows and SIMDs.  Each wave runs a loop
 // specialised for its number of live blocks, so the loop body has no branches.
-template <int GM, bool A_T, bool B_T, int EPI, int BM, int BN, int WM, int WN, int STAGES, int SW, int BK>
+template <int GM, bool A_T, bool B_T, int EPI, int BM, int BN, int WM, int WN, int STAGES, int SW, int BK,
+          int STO = STORE_DIRECT>
 __global__ void __launch_bounds__(64 * WM * WN)
 grouped_gemm2(GemmArgs<bf16> p) {
   constexpr int NW = WM * WN, NT = 64 * NW;
@@ -228,11 +245,16 @@ grouped_gemm2(GemmArgs<bf16> p) {
   constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave
   // store instructions of a full tile's epilogue, per wave
   constexpr int SFULL = EPI == EPI_F32 ? TM * TN * 4 : TM * TN * 2 * (EPI == EPI_BIAS_ACT ? 2 : 1);
-  static_assert(TM >= 1 && TM <= 4 && TN >= 1, "tile");
+  static_assert(TM >= 1 && TM <= 5 && TN >= 1, "tile");
+  // GROUP_M tiles taller than 256 rows split each expert's rows evenly (in 32-row
+  // blocks) over its m-tiles, so an expert slightly above a multiple of the tile height
+  // gets no nearly empty last tile
+  constexpr bool BAL = GM == GROUP_M && BM > 256;
   static_assert(KK % 2 == 0, "fragment slots alternate over an even number of steps");
   static_assert(TA::INSTR % NW == 0 && TB::INSTR % NW == 0, "equal load counts per wave");
   static_assert(GM == GROUP_M || (A_T && B_T), "GROUP_K takes both operands stored per token");
   static_assert(STAGES * LPS <= 63, "vmcnt range");
+  static_assert(STO == STORE_DIRECT || (EPI != EPI_F32 && WTN % 64 == 0), "staged stores: bf16 output, 64-col pieces");
 
   extern __shared__ __align__(1024) char smem[];
   const int tid = threadIdx.x;
@@ -280,8 +302,16 @@ grouped_gemm2(GemmArgs<bf16> p) {
     const int cnt = ld_plan(p.offsets, t.e + 1) - t.off;
     if constexpr (GM == GROUP_M) {
       const int mt_e = (cnt + BM - 1) / BM;
-      t.m0 = (q % mt_e) * BM; t.n0 = (q / mt_e) * BN;
-      t.mvalid = cnt - t.m0; t.kvalid = p.K;
+      if constexpr (BAL) {
+        const int bpt = ((cnt + 31) / 32 + mt_e - 1) / mt_e;   // 32-row blocks per m-tile
+        t.m0 = (q % mt_e) * bpt * 32;
+        t.mvalid = cnt - t.m0 < bpt * 32 ? cnt - t.m0 : bpt * 32;
+      } else {
+        t.m0 = (q % mt_e) * BM;
+        t.mvalid = cnt - t.m0;
+      }
+      t.n0 = (q / mt_e) * BN;
+      t.kvalid = p.K;
       t.Ab = p.A + (int64_t)(t.off + t.m0) * p.lda;
       t.Bb = p.B + (int64_t)t.e * p.b_gstride + (B_T ? (int64_t)t.n0 : (int64_t)t.n0 * p.ldb);
     } else {
@@ -451,6 +481,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
     else if (TM >= 2 && nl == 1) mainloop(std::integral_constant<int, 1>{});
     else if (TM >= 3 && nl == 2) mainloop(std::integral_constant<int, (TM >= 3 ? 2 : 1)>{});
     else if (TM >= 4 && nl == 3) mainloop(std::integral_constant<int, (TM >= 4 ? 3 : 1)>{});
+    else if (TM >= 5 && nl == 4) mainloop(std::integral_constant<int, (TM >= 5 ? 4 : 1)>{});
     else mainloop(std::integral_constant<int, 0>{});
 
     block_sync_lds();      // every wave is done with the ring before the next tile's loads
@@ -516,6 +547,86 @@ grouped_gemm2(GemmArgs<bf16> p) {
             const int nl_ = wn * WTN + i * 32 + 8 * g + 4 * lhi;
             aux_v[i][g] = *reinterpret_cast<const uint2*>(src + arow + n0 + (nl_ < nvalid ? nl_ : 0));
           }
+      }
+      if constexpr (STO != STORE_DIRECT) {
+        // 64 output columns (two 32-column blocks) at a time through the wave's staging
+        // area: lane (row l32, half lhi) writes its 4 x 8 bytes of each block, then lane
+        // L reads row L/8 + 8q, chunk L%8, and stores the whole 128-byte line piece.
+        char* stg = smem + STAGES * SBYTES + wave * STG_WAVE_BYTES;
+        const int rb = (j * WM + wm) * 32;
+        auto stage_out = [&](const uint32_t (&q)[2][4][2], bf16* out, int h) {
+#pragma unroll
+          for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+              *reinterpret_cast<uint2*>(stg + stg_off(l32, 4 * ii + g) + lhi * 8) = make_uint2(q[ii][g][0], q[ii][g][1]);
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+          for (int qd = 0; qd < 4; ++qd) {
+            const int r = (lane >> 3) + 8 * qd, c = lane & 7;
+            const uint4 v = *reinterpret_cast<const uint4*>(stg + stg_off(r, c));
+            const int ml = rb + r, col = wn * WTN + 64 * h + 8 * c;
+            int64_t orow;
+            if constexpr (GM == GROUP_M) orow = (int64_t)(off + m0 + ml) * p.ldc;
+            else orow = (int64_t)e * p.c_gstride + (int64_t)(m0 + ml) * p.ldc;
+            if (ml < mvalid && col < nvalid) {
+              uint4* dst = reinterpret_cast<uint4*>(out + orow + n0 + col);
+              if constexpr (STO == STORE_STAGED_NT) {
+                typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+                __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(dst));
+              } else {
+                *dst = v;
+              }
+            }
+          }
+        };
+#pragma unroll
+        for (int h = 0; h < TN / 2; ++h) {
+          uint32_t pk2[2][4][2], pa2[2][4][2];
+#pragma unroll
+          for (int ii = 0; ii < 2; ++ii) {
+            const int i = 2 * h + ii;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int nl_ = wn * WTN + i * 32 + 8 * g + 4 * lhi;
+              float v[4];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * g + r];
+              if constexpr (HAS_BIAS) {
+                const uint2 b = bias_v[i][g];
+                v[0] += __uint_as_float(b.x << 16); v[1] += __uint_as_float(b.x & 0xffff0000u);
+                v[2] += __uint_as_float(b.y << 16); v[3] += __uint_as_float(b.y & 0xffff0000u);
+              }
+              if constexpr (EPI == EPI_DACT) {
+                const uint2 hv = aux_v[i][g];
+                v[0] *= act_bwd_fast(__uint_as_float(hv.x << 16), p.act);
+                v[1] *= act_bwd_fast(__uint_as_float(hv.x & 0xffff0000u), p.act);
+                v[2] *= act_bwd_fast(__uint_as_float(hv.y << 16), p.act);
+                v[3] *= act_bwd_fast(__uint_as_float(hv.y & 0xffff0000u), p.act);
+              }
+              if constexpr (EPI == EPI_SGD) {
+                const uint2 wv = aux_v[i][g];
+                v[0] = __uint_as_float(wv.x << 16) - p.lr * v[0];
+                v[1] = __uint_as_float(wv.x & 0xffff0000u) - p.lr * v[1];
+                v[2] = __uint_as_float(wv.y << 16) - p.lr * v[2];
+                v[3] = __uint_as_float(wv.y & 0xffff0000u) - p.lr * v[3];
+              }
+              (void)nl_;
+              pk2[ii][g][0] = f2bf2(v[0], v[1]);
+              pk2[ii][g][1] = f2bf2(v[2], v[3]);
+              if constexpr (EPI == EPI_BIAS_ACT) {
+                float a[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) a[r] = act_fwd_fast(v[r], p.act);
+                pa2[ii][g][0] = f2bf2(a[0], a[1]);
+                pa2[ii][g][1] = f2bf2(a[2], a[3]);
+              }
+            }
+          }
+          stage_out(pk2, reinterpret_cast<bf16*>(p.C), h);
+          if constexpr (EPI == EPI_BIAS_ACT) stage_out(pa2, reinterpret_cast<bf16*>(p.C2), h);
+        }
+        continue;
       }
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
@@ -603,9 +714,9 @@ grouped_gemm2(GemmArgs<bf16> p) {
   }
 }
 
-template <int BM, int BN, int STAGES, bool A_T, bool B_T, int BK>
+template <int BM, int BN, int STAGES, bool A_T, bool B_T, int BK, int NW = 8, int STO = STORE_DIRECT>
 constexpr size_t gemm2_lds_bytes() {
-  return (size_t)STAGES * (BM + BN) * BK * 2;
+  return (size_t)STAGES * (BM + BN) * BK * 2 + (STO != STORE_DIRECT ? (size_t)NW * STG_WAVE_BYTES : 0);
 }
 
 }  // namespace dmoe

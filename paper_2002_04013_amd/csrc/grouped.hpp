@@ -3,6 +3,8 @@
 // GEMM implementations (gemm.hpp: fp32; gemm2.hpp: bf16 on gfx950).
 #pragma once
 #include <algorithm>
+#include <atomic>
+#include <cstdio>
 
 #include "common.hpp"
 #include "gemm.hpp"
@@ -105,16 +107,36 @@ static int current_device() {
   return dev;
 }
 
+// Process state of the library: per device, the compute-unit count and each GEMM
+// kernel's resident blocks per compute unit, queried on first use.  Slots are atomics
+// (0 = not yet known); threads that race on a first query store the same value.
 static int device_cus() {
-  static int cus[MAX_DEVICES] = {0};
+  static std::atomic<int> cus[MAX_DEVICES];
   const int dev = current_device();
   if (dev < 0) return 256;
-  if (!cus[dev]) {
+  int c = cus[dev].load(std::memory_order_relaxed);
+  if (!c) {
     int v = 0;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) v = 0;
-    cus[dev] = v > 0 ? v : 256;
+    c = v > 0 ? v : 256;
+    cus[dev].store(c, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return c;
+}
+
+// Resident blocks per compute unit of kernel `kern` with `nt` threads and `lds` bytes
+// of dynamic LDS, cached in `slot` (one per kernel instantiation and device); opts the
+// kernel into dynamic LDS beyond 64 KiB first.
+static int blocks_per_cu(std::atomic<int>* slots, const void* kern, int nt, size_t lds) {
+  const int dev = current_device();
+  int nb = dev >= 0 ? slots[dev].load(std::memory_order_relaxed) : 0;
+  if (!nb) {
+    if (lds > 65536) (void)hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, nt, lds) != hipSuccess || nb < 1) nb = 1;
+    (void)hipGetLastError();
+    if (dev >= 0) slots[dev].store(nb, std::memory_order_relaxed);
+  }
+  return nb;
 }
 
 template <typename E, int GM, bool B_KC, int EPI, int BM, int BN, int BK, int WM, int WN>
@@ -123,41 +145,38 @@ static void run_gemm(GemmArgs<E> p, int64_t tiles_ub, hipStream_t st) {
   auto kern = grouped_gemm<E, GM, B_KC, EPI, BM, BN, BK, WM, WN>;
   constexpr int NT = 64 * WM * WN;
   const size_t lds = gemm_lds_bytes<E, BM, BN, BK, WM, WN>();
-  static int per_cu[MAX_DEVICES] = {0};       // resident blocks per compute unit, per device
-  const int dev = current_device();
-  int nb = dev >= 0 ? per_cu[dev] : 0;
-  if (!nb) {
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, NT, lds) != hipSuccess || nb < 1) nb = 1;
-    (void)hipGetLastError();
-    if (dev >= 0) per_cu[dev] = nb;
-  }
+  static std::atomic<int> per_cu[MAX_DEVICES];
+  static const char* name = [] {
+    static char b[96];
+    snprintf(b, sizeof b, "grouped_gemm<GM=%d,EPI=%d,%dx%d>", GM, EPI, BM, BN);
+    return b;
+  }();
+  const int nb = blocks_per_cu(per_cu, (const void*)kern, NT, lds);
   const int64_t resident = (int64_t)nb * device_cus();
   const int grid = (int)std::min<int64_t>(tiles_ub, resident);
   p.chunked = grid >= 8;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
+  DMOE_LAUNCH_NAMED(name, kern, dim3(grid), dim3(NT), lds, st, p);
 }
 
 // gfx950 bf16 path: direct-to-LDS multi-stage GEMM (gemm2.hpp)
-template <int GM, bool AT, bool BT, int EPI, int BM, int BN, int WM, int WN, int ST, int BK>
+template <int GM, bool AT, bool BT, int EPI, int BM, int BN, int WM, int WN, int ST, int BK, int STO = STORE_DIRECT>
 static void run_gemm2(GemmArgs<bf16> p, int64_t tiles_ub, hipStream_t st) {
   if (tiles_ub <= 0) return;
-  auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1, BK>;
+  auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1, BK, STO>;
   constexpr int NT = 64 * WM * WN;
-  const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT, BK>();
-  static int per_cu[MAX_DEVICES] = {0};       // resident blocks per compute unit, per device
-  const int dev = current_device();
-  int nb = dev >= 0 ? per_cu[dev] : 0;
-  if (!nb) {
-    // dynamic LDS beyond 64 KiB is opted into per kernel, on the current device
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, NT, lds) != hipSuccess || nb < 1) nb = 1;
-    (void)hipGetLastError();
-    if (dev >= 0) per_cu[dev] = nb;
-  }
+  const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT, BK, WM * WN, STO>();
+  static std::atomic<int> per_cu[MAX_DEVICES];
+  static const char* name = [] {
+    static char b[96];
+    snprintf(b, sizeof b, "grouped_gemm2<GM=%d,AT=%d,BT=%d,EPI=%d,%dx%d,ST=%d,BK=%d>", GM, (int)AT, (int)BT, EPI, BM,
+             BN, ST, BK);
+    return b;
+  }();
+  const int nb = blocks_per_cu(per_cu, (const void*)kern, NT, lds);
   const int64_t resident = (int64_t)nb * device_cus();
   const int grid = (int)std::min<int64_t>(tiles_ub, resident);
   p.chunked = grid >= 8;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), lds, st, p);
+  DMOE_LAUNCH_NAMED(name, kern, dim3(grid), dim3(NT), lds, st, p);
 }
 
 template <typename E>
@@ -178,10 +197,15 @@ struct CfgDWF32  { static constexpr int BM = 64, BN = 64, BK = 32, WM = 2, WN = 
 // many rows, 32-deep ones when they hold few (a k-step past an expert's last row is
 // zero-filled in LDS and still multiplied, so with ~16 rows per expert a 64-deep step
 // spends three quarters of its MFMA and LDS reads on zeros).
+// Weight-gradient tiles write their 128 KiB of output through LDS as whole 128-byte
+// lines with the non-temporal hint: the 64 GiB of weight gradients per step then
+// stream past the L2 instead of evicting the GEMM's operands from it.
 struct G2Fat     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
 struct G2Skinny  { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4, BK = 64; };
-struct G2DW      { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
-struct G2DWShort { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 4, BK = 32; };
+struct G2DW      { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64,
+                   STO = STORE_STAGED_NT; };
+struct G2DWShort { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 4, BK = 32,
+                   STO = STORE_STAGED_NT; };
 
 static bool use_fat(const Shape& s) { return s.P >= (int64_t)96 * s.N; }
 

@@ -293,20 +293,20 @@ extern "C" int dmoe_dispatch(const dmoe_dims* dims, const void* x, const int32_t
   const int N = (int)s.N, P = (int)s.P;
   const int nb = (int)L.disp_blocks;
   if (nb > 0)
-    hipLaunchKernelGGL(dispatch_hist, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N, bh);
-  hipLaunchKernelGGL(dispatch_scan_cols, dim3((N + SCAN_E - 1) / SCAN_E), dim3(SCAN_E * SCAN_S), 0, st, bh, nb,
+    DMOE_LAUNCH(dispatch_hist, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N, bh);
+  DMOE_LAUNCH(dispatch_scan_cols, dim3((N + SCAN_E - 1) / SCAN_E), dim3(SCAN_E * SCAN_S), 0, st, bh, nb,
                      N, counts);
-  hipLaunchKernelGGL(dispatch_scan_offsets, dim3(1), dim3(1024), 0, st, counts, N, offsets);
+  DMOE_LAUNCH(dispatch_scan_offsets, dim3(1), dim3(1024), 0, st, counts, N, offsets);
   if (nb == 0) return launch_status();
-  hipLaunchKernelGGL(dispatch_scatter, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N,
+  DMOE_LAUNCH(dispatch_scatter, dim3(nb), dim3(RT_NT), N * sizeof(int), st, idx, alive, P, N,
                      s.k, bh, offsets, pos, row_token);
   const int64_t chunks = s.T * (s.D * (int64_t)s.esz / 16);
   const int grid = (int)std::min<int64_t>((chunks + RT_NT - 1) / RT_NT, 256 * 16);
   if (s.dtype == DMOE_BF16)
-    hipLaunchKernelGGL(gather_rows<bf16>, dim3(grid), dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(x),
+    DMOE_LAUNCH(gather_rows<bf16>, dim3(grid), dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(x),
                        pos, (int)s.T, s.k, (int)s.D, reinterpret_cast<bf16*>(x_perm));
   else
-    hipLaunchKernelGGL(gather_rows<float>, dim3(grid), dim3(RT_NT), 0, st, reinterpret_cast<const float*>(x),
+    DMOE_LAUNCH(gather_rows<float>, dim3(grid), dim3(RT_NT), 0, st, reinterpret_cast<const float*>(x),
                        pos, (int)s.T, s.k, (int)s.D, reinterpret_cast<float*>(x_perm));
   return launch_status();
 }
@@ -322,10 +322,10 @@ extern "C" int dmoe_combine(const dmoe_dims* dims, const void* y_perm, const int
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((unsigned)((s.T + 3) / 4));
   if (s.dtype == DMOE_BF16)
-    hipLaunchKernelGGL(combine_kernel<bf16>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(y_perm),
+    DMOE_LAUNCH(combine_kernel<bf16>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(y_perm),
                        pos, w, reinterpret_cast<bf16*>(y), (int)s.T, (int)s.D, s.k);
   else
-    hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const float*>(y_perm),
+    DMOE_LAUNCH(combine_kernel<float>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const float*>(y_perm),
                        pos, w, reinterpret_cast<float*>(y), (int)s.T, (int)s.D, s.k);
   return launch_status();
 }
@@ -342,11 +342,11 @@ extern "C" int dmoe_combine_bwd(const dmoe_dims* dims, const void* dy, const voi
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((unsigned)((s.T + 3) / 4));
   if (s.dtype == DMOE_BF16)
-    hipLaunchKernelGGL(combine_bwd_kernel<bf16>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(dy),
+    DMOE_LAUNCH(combine_bwd_kernel<bf16>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(dy),
                        reinterpret_cast<const bf16*>(y_perm), pos, w, reinterpret_cast<bf16*>(dy_perm), dw,
                        (int)s.T, (int)s.D, s.k);
   else
-    hipLaunchKernelGGL(combine_bwd_kernel<float>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const float*>(dy),
+    DMOE_LAUNCH(combine_bwd_kernel<float>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const float*>(dy),
                        reinterpret_cast<const float*>(y_perm), pos, w, reinterpret_cast<float*>(dy_perm), dw,
                        (int)s.T, (int)s.D, s.k);
   return launch_status();
@@ -365,12 +365,12 @@ extern "C" int dmoe_dispatch_bwd(const dmoe_dims* dims, const void* dx_perm, con
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((unsigned)((s.T + 3) / 4));
   if (s.dtype == DMOE_BF16)
-    hipLaunchKernelGGL(dispatch_bwd_kernel<bf16>, grid, dim3(RT_NT), 0, st,
+    DMOE_LAUNCH(dispatch_bwd_kernel<bf16>, grid, dim3(RT_NT), 0, st,
                        reinterpret_cast<const bf16*>(dx_perm), pos, gate ? idx : nullptr, gate ? dg : nullptr,
                        reinterpret_cast<const bf16*>(Wg), reinterpret_cast<bf16*>(dx), (int)s.T, (int)s.D, s.k,
                        s.d, s.M);
   else
-    hipLaunchKernelGGL(dispatch_bwd_kernel<float>, grid, dim3(RT_NT), 0, st,
+    DMOE_LAUNCH(dispatch_bwd_kernel<float>, grid, dim3(RT_NT), 0, st,
                        reinterpret_cast<const float*>(dx_perm), pos, gate ? idx : nullptr, gate ? dg : nullptr,
                        reinterpret_cast<const float*>(Wg), reinterpret_cast<float*>(dx), (int)s.T, (int)s.D, s.k,
                        s.d, s.M);
