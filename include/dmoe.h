@@ -159,6 +159,20 @@ int dmoe_expert_ffn_fwd(const dmoe_dims* dims, const int32_t* offsets, const voi
                         const void* W1, const void* b1, const void* W2, const void* b2,
                         void* h, void* a, void* y_perm, void* ws, void* stream);
 
+/* dmoe_expert_ffn_fwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, results and kernels as dmoe_expert_ffn_fwd, bit
+ * for bit; its only scratch, the tile plan (2 (N + 1) int32, at most 131328 bytes for
+ * N <= 16384), lives in a static device array of the library that each GPU holds until
+ * the process ends.  It calls no allocating routine.  Every call on one GPU uses that
+ * GPU's copy of the array, so calls that overlap on one GPU (different streams, or other
+ * host threads) race and must not be issued; calls in sequence on one stream are fine.
+ * Returns DMOE_EUNSUPPORTED if the tile plan would exceed the array, DMOE_EHIP if its
+ * device address cannot be obtained. */
+int dmoe_expert_ffn_fwd_noalloc(const dmoe_dims* dims, const int32_t* offsets, const void* x_perm,
+                                const void* W1, const void* b1, const void* W2, const void* b2,
+                                void* h, void* a, void* y_perm, void* stream);
+
 /* Weighted average of Eq. 1:  y[t] = sum_j w[t,j] y_perm[pos[t,j]] over pairs with
  * pos >= 0, in slot order, fp32 accumulation.  y [T, D] written (zeros for tokens
  * with no alive expert).  Uses workspace: no. */

@@ -24,7 +24,7 @@ EXPORTS = (
     "dmoe_expert_ffn_fwd", "dmoe_combine", "dmoe_combine_bwd", "dmoe_gate_topk_bwd",
     "dmoe_expert_ffn_bwd", "dmoe_dispatch_bwd", "dmoe_expert_ffn_bwd_recompute", "dmoe_expert_ffn_bwd_sgd",
     "dmoe_expert_ffblock_fwd", "dmoe_expert_ffblock_bwd", "dmoe_ln_act_fwd", "dmoe_ln_act_bwd",
-    "dmoe_trace_begin", "dmoe_trace_end",
+    "dmoe_trace_begin", "dmoe_trace_end", "dmoe_expert_ffn_fwd_noalloc",
 )
 
 # parameters of the feed-forward block expert, in dmoe_ffblock_params order
@@ -92,6 +92,7 @@ def load(path=LIB_PATH):
         "dmoe_trace_begin": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_char_p),
                                             ctypes.c_int]),
         "dmoe_trace_end": (ctypes.c_int, []),
+        "dmoe_expert_ffn_fwd_noalloc": (ctypes.c_int, [pd] + [_P] * 10),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -148,6 +149,12 @@ def dmoe_expert_ffn_fwd(dims, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm, ws,
     _check(load().dmoe_expert_ffn_fwd(ctypes.byref(dims), _ptr(offsets), _ptr(x_perm), _ptr(W1),
                                       _ptr(b1), _ptr(W2), _ptr(b2), _ptr(h), _ptr(a), _ptr(y_perm),
                                       _ptr(ws), _stream(stream)), "dmoe_expert_ffn_fwd")
+
+
+def dmoe_expert_ffn_fwd_noalloc(dims, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm, stream=None):
+    _check(load().dmoe_expert_ffn_fwd_noalloc(ctypes.byref(dims), _ptr(offsets), _ptr(x_perm), _ptr(W1),
+                                              _ptr(b1), _ptr(W2), _ptr(b2), _ptr(h), _ptr(a), _ptr(y_perm),
+                                              _stream(stream)), "dmoe_expert_ffn_fwd_noalloc")
 
 
 def dmoe_combine(dims, y_perm, pos, w, y, stream=None):

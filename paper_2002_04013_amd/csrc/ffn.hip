@@ -266,23 +266,10 @@ static void ffn_up_cfg(const Shape& s, const int32_t* offsets, const E* xp, cons
   run_gemm<E, GROUP_M, true, EPI_BIAS_ACT, C::BM, C::BN, C::BK, C::WM, C::WN>(p, mt_ub * nt, st);
 }
 
-}  // namespace dmoe
-
-using namespace dmoe;
-
-extern "C" int dmoe_expert_ffn_fwd(const dmoe_dims* dims, const int32_t* offsets, const void* x_perm,
-                                   const void* W1, const void* b1, const void* W2, const void* b2,
-                                   void* h, void* a, void* y_perm, void* ws, void* stream) {
-  Shape s;
-  int rc = check_dims(dims, &s);
-  if (rc) return rc;
-  if (s.T == 0) return DMOE_OK;
-  if (!offsets || !x_perm || !W1 || !b1 || !W2 || !b2 || !h || !a || !y_perm || !ws) return DMOE_EINVAL;
-  for (const void* q : {x_perm, W1, W2, (const void*)h, (const void*)a, (const void*)y_perm, (const void*)ws})
-    if (!aligned16(q)) return DMOE_EUNSUPPORTED;
-  const Workspace L = workspace_layout(s);
-  int32_t* tpre = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + L.tiles_off);
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+// The forward on a tile plan at tpre (2 (N + 1) ints of device memory).
+static int ffn_fwd_impl(const Shape& s, const int32_t* offsets, const void* x_perm, const void* W1,
+                        const void* b1, const void* W2, const void* b2, void* h, void* a, void* y_perm,
+                        int32_t* tpre, hipStream_t st) {
   if (s.dtype == DMOE_BF16) {
     auto c = [](const void* q) { return reinterpret_cast<const bf16*>(q); };
     auto m = [](void* q) { return reinterpret_cast<bf16*>(q); };
@@ -296,6 +283,70 @@ extern "C" int dmoe_expert_ffn_fwd(const dmoe_dims* dims, const int32_t* offsets
     ffn_fwd_cfg<float, CfgF32>(s, offsets, c(x_perm), c(W1), c(b1), c(W2), c(b2), m(h), m(a), m(y_perm), tpre, st);
   }
   return launch_status();
+}
+
+static int ffn_fwd_check(const dmoe_dims* dims, Shape* s, const int32_t* offsets, const void* x_perm, const void* W1,
+                         const void* b1, const void* W2, const void* b2, const void* h, const void* a,
+                         const void* y_perm) {
+  const int rc = check_dims(dims, s);
+  if (rc) return rc;
+  if (s->T == 0) return DMOE_OK;
+  if (!offsets || !x_perm || !W1 || !b1 || !W2 || !b2 || !h || !a || !y_perm) return DMOE_EINVAL;
+  for (const void* q : {x_perm, W1, W2, h, a, y_perm})
+    if (!aligned16(q)) return DMOE_EUNSUPPORTED;
+  return DMOE_OK;
+}
+
+// Scratch of dmoe_expert_ffn_fwd_noalloc: the tile plan, 2 (N + 1) ints for N <= NMAX.
+// Each device holds its own copy; host code reaches it only through the address
+// hipGetSymbolAddress returns on that device (the array's name is no device address
+// in host code).
+constexpr size_t FFN_SCRATCH_BYTES = ((size_t)2 * (NMAX + 1) * sizeof(int32_t) + 255) & ~(size_t)255;
+static __device__ __align__(256) unsigned char scratch[FFN_SCRATCH_BYTES];
+
+// scratch's address on the current device, looked up on the first call there.
+static int32_t* scratch_on_device() {
+  static std::atomic<void*> addr[MAX_DEVICES];
+  const int dev = current_device();
+  if (dev < 0) return nullptr;
+  void* p = addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    addr[dev].store(p, std::memory_order_release);
+  }
+  return reinterpret_cast<int32_t*>(p);
+}
+
+}  // namespace dmoe
+
+using namespace dmoe;
+
+extern "C" int dmoe_expert_ffn_fwd(const dmoe_dims* dims, const int32_t* offsets, const void* x_perm,
+                                   const void* W1, const void* b1, const void* W2, const void* b2,
+                                   void* h, void* a, void* y_perm, void* ws, void* stream) {
+  Shape s;
+  int rc = ffn_fwd_check(dims, &s, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm);
+  if (rc || s.T == 0) return rc;
+  if (!ws) return DMOE_EINVAL;
+  if (!aligned16(ws)) return DMOE_EUNSUPPORTED;
+  const Workspace L = workspace_layout(s);
+  int32_t* tpre = reinterpret_cast<int32_t*>(reinterpret_cast<unsigned char*>(ws) + L.tiles_off);
+  return ffn_fwd_impl(s, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm, tpre, reinterpret_cast<hipStream_t>(stream));
+}
+
+extern "C" int dmoe_expert_ffn_fwd_noalloc(const dmoe_dims* dims, const int32_t* offsets, const void* x_perm,
+                                           const void* W1, const void* b1, const void* W2, const void* b2,
+                                           void* h, void* a, void* y_perm, void* stream) {
+  Shape s;
+  int rc = ffn_fwd_check(dims, &s, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm);
+  if (rc || s.T == 0) return rc;
+  if ((size_t)2 * (s.N + 1) * sizeof(int32_t) > FFN_SCRATCH_BYTES) return DMOE_EUNSUPPORTED;
+  int32_t* tpre = scratch_on_device();
+  if (!tpre) return DMOE_EHIP;
+  return ffn_fwd_impl(s, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm, tpre, reinterpret_cast<hipStream_t>(stream));
 }
 
 extern "C" int dmoe_expert_ffn_bwd(const dmoe_dims* dims, const int32_t* offsets, const int32_t* counts,
