@@ -1,16 +1,26 @@
 #!/usr/bin/env python3
 """Benchmark of one DMoE layer, forward + backward, on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload wide]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload wide] [--no-extra]
 
 A step is one pass of the whole layer over one batch of synthetic input:
 gate + TopK + weights, dispatch, expert FFN forward, combine, and the backward of
 all of them (combine, gate, expert FFN, dispatch).  Inputs and weights are
 resident in HBM before the timed region.  Prints one JSON line.
+
+Inside the timed region every kernel the library enqueues is timed with HIP events
+on its stream (the library's launch trace), so the line reports each kernel's
+per-launch duration and roofline fraction and names the kernel that takes the most
+time per step.  After the timed region a cold pass flushes the memory-side cache
+before each step and times the gate and the dispatch again.  The other workloads
+(1024- and 4096-expert layers, the LayerNorm block experts, the tiny fp32 layer)
+are then timed for a few steps each and reported under "workloads".
 """
 import argparse
+import gc
 import json
 import os
+import re
 import sys
 import time
 
@@ -25,6 +35,20 @@ PEAK_HBM_GBS = 8000.0
 CALLS = ("gate_topk", "dispatch", "ffn_fwd", "combine", "combine_bwd", "gate_topk_bwd", "ffn_bwd",
          "dispatch_bwd")
 FWD_CALLS = ("gate_topk", "dispatch", "ffn_fwd", "combine")
+EXTRA_WORKLOADS = ("tfm_fwd", "tfm_fail_skew", "grid3d", "ffblock", "tiny_f32")
+COLD_WORKLOADS = ("wide", "grid3d")
+FLUSH_BYTES = 1 << 30          # memory-side cache flush: 1 GiB written, then 1 GiB read
+
+# The paper's own throughput figure, reported beside the result as context only: it is
+# system-level training over the internet, not a single-GPU layer measurement.
+PAPER_CONTEXT = {
+    "value": "300.8 +- 15.9 samples/s",
+    "what": ("Learning@home training throughput, 224 feed-forward blocks 1024-4096-4096-1024 with "
+             "LayerNorm and ReLU, batch 2048, 64 trainers (Sec. 4.1, Table 2)"),
+    "hardware": "3 cloud Tesla K80 instances in three regions, network latency 92.49 +- 32.42 ms",
+    "model_parallel_same_setup": "7.23 +- 0.06 samples/s",
+    "note": "context, not the target: a different machine, precision and measurement",
+}
 
 
 def algorithmic(wl, counts, recompute=False, sgd=False):
@@ -74,19 +98,77 @@ def algorithmic_block(wl, counts):
             "ffn_bwd": dict(bytes=3 * wbytes + bwd_rows, flops=2 * flops)}
 
 
-def cpu_baseline(wl, inp, counts, budget_s=12.0):
-    """The oracle, as it stands, on a bounded sample of the same workload: routing
-    (gate, TopK, weights), dispatch and the gate backward for every token, then the
-    expert blocks forward+backward for a few experts, extrapolated linearly in pairs
-    to the whole batch."""
-    import numpy as np
-    import oracle as O
+_GEMM2 = re.compile(r"grouped_gemm2<GM=(\d),AT=(\d),BT=(\d),EPI=(\d)")
+
+
+def kernel_algorithmic(name, wl, counts, sgd=False):
+    """(role, flops, bytes) of one launch of kernel `name` in a Linear-act-Linear layer,
+    or None for kernels without a per-launch closed form here.  A grouped GEMM launch
+    multiplies every alive pair's row once (2 rows D H flops) and reads each touched
+    expert's weight matrix once; the per-row operands and outputs are read or written
+    once."""
+    if wl.expert != "ffn":
+        return None
+    e = 2 if wl.dtype == "bf16" else 4
+    T, D, H, k, dM = wl.T, wl.D, wl.H, wl.k, wl.dM
+    rows = int(sum(counts))
+    touched = int(sum(1 for c in counts if c > 0))
+    w = touched * D * H * e
+    f = 2 * rows * D * H
+    m = _GEMM2.match(name)
+    if m:
+        gm, bt, epi = int(m.group(1)), int(m.group(3)), int(m.group(4))
+        if gm == 1:       # weight gradient: read the rows of both operands, write dW (SGD: read W too)
+            return "expert weight-gradient GEMM", f, rows * (D + H) * e + (2 * w if epi == 5 else w)
+        if epi == 2:      # up-projection with bias and activation: read x_perm, W1, b1; write h and a
+            return "expert up-projection GEMM", f, w + touched * H * e + rows * (D + 2 * H) * e
+        if epi == 1:      # down-projection with bias: read a, W2, b2; write y_perm
+            return "expert down-projection GEMM", f, w + touched * D * e + rows * (H + D) * e
+        if epi == 3:      # dh = (dy W2) act'(h): read dy_perm, W2, h; write dh
+            return "expert dh GEMM", f, w + rows * (D + 2 * H) * e
+        if epi == 0 and bt == 1:   # dx_perm = dh W1: read dh, W1; write dx_perm
+            return "expert dx GEMM", f, w + rows * (H + D) * e
+        return None
+    if name.startswith("gate_topk_mfma"):
+        return "gate scores + TopK (MFMA)", 2 * T * D * dM, T * D * e + dM * D * e + T * k * 12
+    if name.startswith("gather_rows"):
+        return "dispatch row gather", 0, T * D * e + rows * D * e
+    if name.startswith("combine_kernel"):
+        return "combine", 2 * rows * D, rows * D * e + T * D * e + T * k * 8
+    if name.startswith("combine_bwd_kernel"):
+        return "combine backward", 4 * rows * D, T * D * e + 2 * rows * D * e + T * k * 8
+    if name.startswith("dispatch_bwd_kernel"):
+        return "dispatch backward", 0, rows * D * e + T * D * e + T * k * 8
+    return None
+
+
+def roofline_of(flops, nbytes, seconds, peak_tf):
+    ridge = peak_tf * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if flops and flops / max(nbytes, 1) >= ridge:
+        ach = flops / seconds / 1e12
+        return {"bound": "mfma", "achieved": round(ach, 1), "peak": peak_tf, "unit": "TFLOP/s",
+                "frac": round(ach / peak_tf, 4)}
+    ach = nbytes / seconds / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(ach / PEAK_HBM_GBS, 4)}
+
+
+def blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
-                      or [1])
+        return max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
     except Exception:
-        threads = os.cpu_count() or 1
+        return os.cpu_count() or 1
+
+
+def cpu_baseline(wl, inp, counts, budget_s=12.0, max_experts=16):
+    """The oracle, as it stands, on a bounded sample of the same workload: routing
+    (gate, TopK, weights), dispatch and (with a backward) the gate backward for every
+    token, then the expert blocks (forward, and backward when the workload has one) for
+    a few experts, extrapolated linearly in pairs to the whole batch."""
+    import numpy as np
+    import oracle as O
+    threads = blas_threads()
     x = O.to64(inp["x"])
     Wg, bg = O.to64(inp["Wg"]), O.to64(inp["bg"])
     alive = inp["alive"].cpu().numpy()
@@ -96,7 +178,8 @@ def cpu_baseline(wl, inp, counts, budget_s=12.0):
     t0 = time.perf_counter()
     r = O.routing(x, Wg, bg, alive, wl.d, wl.M, wl.k)
     c, off, row_token, pos = O.dispatch(r["idx"], alive, N)
-    O.gate_backward(r["w"], np.zeros_like(r["w"]), r["idx"], alive, x, Wg, wl.d, wl.M)
+    if wl.backward:
+        O.gate_backward(r["w"], np.zeros_like(r["w"]), r["idx"], alive, x, Wg, wl.d, wl.M)
     t_route = time.perf_counter() - t0
 
     live = [int(e) for e in np.nonzero(c)[0]]
@@ -110,25 +193,42 @@ def cpu_baseline(wl, inp, counts, budget_s=12.0):
             t1 = time.perf_counter()
             X = x[rows]
             fw = O.ffblock_forward_stored(X, prm, wl.act)
-            O.ffblock_backward(X, fw, dy[rows], prm, wl.act)
+            if wl.backward:
+                O.ffblock_backward(X, fw, dy[rows], prm, wl.act)
         else:
             W1, b1, W2, b2 = (O.to64(inp[n][e]) for n in ("W1", "b1", "W2", "b2"))   # not timed
             t1 = time.perf_counter()
             X = x[rows]
             h, a, y = O.expert_forward(X, W1, b1, W2, b2, wl.act)
-            O.expert_backward(X, h, a, dy[rows], W1, W2, wl.act)
+            if wl.backward:
+                O.expert_backward(X, h, a, dy[rows], W1, W2, wl.act)
         t_exp += time.perf_counter() - t1
         pairs += len(rows)
         used += 1
-        if t_exp + t_route > budget_s or used >= 16:
+        if t_exp + t_route > budget_s or used >= max_experts:
             break
     total_pairs = int(off[-1])
     est = t_route + t_exp * total_pairs / max(pairs, 1)
+    passes = "fwd+bwd" if wl.backward else "fwd"
     return {"value": round(wl.T / est, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"fp64 NumPy oracle: routing, dispatch and gate backward for all {wl.T} tokens "
-                       f"({t_route:.2f} s) + expert fwd+bwd for {used} experts ({pairs} of "
-                       f"{total_pairs} pairs, {t_exp:.2f} s), extrapolated linearly in pairs"),
+            "sample": (f"fp64 NumPy oracle ({passes}) on {threads} BLAS thread(s): routing, dispatch"
+                       f"{' and gate backward' if wl.backward else ''} for all {wl.T} tokens ({t_route:.2f} s) "
+                       f"+ expert {passes} for {used} experts ({pairs} of {total_pairs} pairs, {t_exp:.2f} s), "
+                       f"extrapolated linearly in pairs"),
             "seconds_measured": round(t_route + t_exp, 3)}
+
+
+def cpu_baselines(wl, inp, counts):
+    """The oracle on the host's BLAS threads, then on one thread (smaller sample)."""
+    out = cpu_baseline(wl, inp, counts)
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1, user_api="blas"):
+            one = cpu_baseline(wl, inp, counts, budget_s=8.0, max_experts=4)
+        out["one_thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample", "seconds_measured")}
+    except Exception as ex:  # threadpoolctl missing: report the main figure only
+        out["one_thread"] = {"error": str(ex)}
+    return out
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_wide.json")
@@ -136,8 +236,8 @@ KERNEL_SOURCES = ("gemm.hpp", "gemm2.hpp", "grouped.hpp", "ffn.hip", "common.hpp
 
 
 def kernel_source_hash():
-    """Hash of the sources of the dominant kernel: counter readings are valid only
-    for the exact kernel they were taken on."""
+    """Hash of the GEMM sources: counter readings are valid only for the exact kernels
+    they were taken on."""
     import hashlib
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
@@ -146,10 +246,10 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload):
-    """HBM bytes per dmoe_expert_ffn_fwd call from the committed rocprofv3 counter
-    summary (FETCH_SIZE + WRITE_SIZE of its GEMM launches, scaled by the copy-kernel
-    calibration), or None if there is none for this workload and kernel source."""
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` (FETCH_SIZE + WRITE_SIZE from two rocprofv3
+    counter runs, scaled by the copy-kernel calibration) from the committed counter
+    summary, or None if there is none for this workload, kernel and kernel source."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
@@ -157,7 +257,8 @@ def measured_traffic(workload):
         return None
     if t.get("workload") != workload or t.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return t.get("ffn_fwd_bytes")
+    k = t.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("bytes_per_launch")
 
 
 def copy_calibration(nbytes=4 << 30, reps=5):
@@ -174,13 +275,224 @@ def copy_calibration(nbytes=4 << 30, reps=5):
     print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "reps": reps}), flush=True)
 
 
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def run_workload(name, steps, warmup, recompute=False, sgd=False, alive_topk=False, cold_steps=0,
+                 cpu=False):
+    """Build one workload's inputs and layer, time `steps` steps after `warmup`, trace
+    every kernel in the timed region, optionally time `cold_steps` more steps each after
+    a cache flush, and return the measurements."""
+    import torch
+    from paper_2002_04013_amd import DMoEBlockLayer, DMoELayer, abi
+    from workloads import (get_workload, make_alive, make_block_experts, make_dy, make_experts, make_gate,
+                           make_x)
+
+    wl = get_workload(name)
+    block = wl.expert == "ffblock"
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    Wg, bg = make_gate(wl, dev)
+    inp = dict(x=make_x(wl, dev), dy=make_dy(wl, dev), Wg=Wg, bg=bg, alive=make_alive(wl, dev))
+    dWg, dbg = torch.empty_like(Wg), torch.empty_like(bg)
+    flags = abi.DMOE_FLAG_ALIVE_TOPK if alive_topk else 0
+    if block:
+        prm = make_block_experts(wl, dev)
+        inp["params"] = prm
+        grads = {n: torch.empty_like(v) for n, v in prm.items()}
+        L = DMoEBlockLayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, flags=flags)
+    else:
+        W1, b1, W2, b2 = make_experts(wl, dev)
+        inp.update(W1=W1, b1=b1, W2=W2, b2=b2)
+        dW1, db1 = torch.empty_like(W1), torch.empty_like(b1)
+        dW2, db2 = torch.empty_like(W2), torch.empty_like(b2)
+        L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, dh_aliases_h=False,
+                      flags=flags)
+    torch.cuda.synchronize()
+    log(f"{wl.name}: inputs ready in {time.perf_counter() - t_gen:.1f} s")
+
+    x, alive = inp["x"], inp["alive"]
+    Dm = L.dims
+    stream = torch.cuda.current_stream()
+    calls = [
+        ("gate_topk", lambda: abi.dmoe_gate_topk(Dm, x, Wg, bg, alive, L.idx, L.w, None, None, L.ws)),
+        ("dispatch", lambda: abi.dmoe_dispatch(Dm, x, L.idx, alive, L.counts, L.offsets, L.row_token,
+                                               L.pos, L.x_perm, L.ws)),
+        ("ffn_fwd", (lambda: abi.dmoe_expert_ffblock_fwd(Dm, L.offsets, L.x_perm, prm, L.acts, L.y_perm,
+                                                         L.ws)) if block else
+         (lambda: abi.dmoe_expert_ffn_fwd(Dm, L.offsets, L.x_perm, W1, b1, W2, b2, L.h, L.a,
+                                          L.y_perm, L.ws))),
+        ("combine", lambda: abi.dmoe_combine(Dm, L.y_perm, L.pos, L.w, L.y)),
+        ("combine_bwd", lambda: abi.dmoe_combine_bwd(Dm, inp["dy"], L.y_perm, L.pos, L.w, L.dy_perm, L.dw)),
+        ("gate_topk_bwd", lambda: abi.dmoe_gate_topk_bwd(Dm, x, L.idx, L.w, L.dw, alive, L.dg, dWg, dbg,
+                                                         L.ws)),
+        ("ffn_bwd", (lambda: abi.dmoe_expert_ffblock_bwd(Dm, L.offsets, L.x_perm, prm, L.acts, L.dy_perm,
+                                                         L.g1, L.g2, L.dx_perm, grads, L.ws)) if block else
+         (lambda: abi.dmoe_expert_ffn_bwd_sgd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a, L.dy_perm, W1, b1,
+                                              W2, b2, 1e-4, L.dh, L.dx_perm, L.ws)) if sgd else
+         (lambda: abi.dmoe_expert_ffn_bwd_recompute(Dm, L.offsets, L.counts, L.x_perm, W1, b1, W2,
+                                                    L.dy_perm, L.h, L.a, L.dx_perm, dW1, db1, dW2, db2,
+                                                    L.ws)) if recompute else
+         (lambda: abi.dmoe_expert_ffn_bwd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a, L.dy_perm, W1, W2,
+                                          L.dh, L.dx_perm, dW1, db1, dW2, db2, L.ws))),
+        ("dispatch_bwd", lambda: abi.dmoe_dispatch_bwd(Dm, L.dx_perm, L.pos, L.idx, L.dg, Wg, L.dx)),
+    ]
+    calls = [(n, f) for n, f in calls if wl.backward or n in FWD_CALLS]
+    timed = [n for n, _ in calls]
+
+    def step(ev=None):
+        for n, fn in calls:
+            if ev is not None:
+                ev[n][0].record(stream)
+            fn()
+            if ev is not None:
+                ev[n][1].record(stream)
+
+    def new_events(k):
+        return [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in timed}
+                for _ in range(k)]
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    counts = L.counts.cpu().tolist()
+
+    evs = new_events(steps)
+    trace = abi.Trace(capacity=steps * 64, stream=stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with trace:
+        for i in range(steps):
+            step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in evs) / steps for n in timed}
+    per_step = sorted(e[timed[0]][0].elapsed_time(e[timed[-1]][1]) for e in evs)
+    kern = trace.kernels()
+    log(f"{wl.name}: {steps} steps in {wall:.3f} s; per call ms: " +
+        ", ".join(f"{n} {v:.3f}" for n, v in ms.items()))
+
+    alg = algorithmic(wl, counts, recompute, sgd)
+    if block:
+        alg.update(algorithmic_block(wl, counts))
+    peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+
+    # per-kernel table from the trace
+    agg = {}
+    for kname, t in kern:
+        a = agg.setdefault(kname, [0, 0.0])
+        a[0] += 1
+        a[1] += t
+    kernels = []
+    for kname, (n, t) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        row = {"name": kname, "launches_per_step": round(n / steps, 3), "ms_per_step": round(t / steps, 4),
+               "ms_per_launch": round(t / n, 4)}
+        ka = kernel_algorithmic(kname, wl, counts, sgd)
+        if ka is not None:
+            role, fl, nb = ka
+            row.update(role=role, flops_per_launch=fl, bytes_per_launch=nb)
+            row.update(roofline_of(fl, nb, t / n * 1e-3, peak_tf))
+        kernels.append(row)
+
+    def call_roof(n):
+        a = alg[n]
+        return roofline_of(a["flops"], a["bytes"], ms[n] * 1e-3, peak_tf)
+
+    out = {"wl": wl, "counts": counts, "wall": wall, "ms": ms, "per_step": per_step, "kernels": kernels,
+           "call_roofline": {n: call_roof(n) for n in timed}, "alg": alg, "peak_tf": peak_tf,
+           "traced": trace.count, "inp_host": None}
+
+    if cold_steps:
+        # Cold memory-side cache: before each step, outside any timed interval, write
+        # FLUSH_BYTES to one scratch buffer and read FLUSH_BYTES from another, so the
+        # step's first reads (the gate's x) come from HBM and no dirty lines of the
+        # previous step are left to write back.
+        fw = torch.empty(FLUSH_BYTES // 2, dtype=torch.int16, device=dev)
+        fr = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+        cev = new_events(cold_steps)
+        ctrs = [abi.Trace(capacity=64, stream=stream) for _ in range(cold_steps)]
+        sink = torch.zeros((), dtype=torch.float32, device=dev)
+        for i in range(cold_steps):
+            fw.fill_(i)
+            sink += fr.sum()
+            with ctrs[i]:
+                step(cev[i])
+        torch.cuda.synchronize()
+        cms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in cev) / cold_steps for n in ("gate_topk", "dispatch")}
+        ck = {}
+        for ctr in ctrs:
+            for kname, t in ctr.kernels():
+                if kname.startswith("gate_topk_mfma") or kname.startswith("gather_rows"):
+                    ck.setdefault(kname, []).append(t)
+        cold = {}
+        for n in ("gate_topk", "dispatch"):
+            warm_r, cold_r = call_roof(n), roofline_of(alg[n]["flops"], alg[n]["bytes"], cms[n] * 1e-3, peak_tf)
+            cold[n] = {"warm_ms": round(ms[n], 4), "cold_ms": round(cms[n], 4),
+                       "warm_frac": warm_r["frac"], "cold_frac": cold_r["frac"], "bound": cold_r["bound"],
+                       "cold_achieved": cold_r["achieved"], "unit": cold_r["unit"]}
+        for kname, ts in ck.items():
+            ka = kernel_algorithmic(kname, wl, counts)
+            t = sum(ts) / len(ts)
+            r = roofline_of(ka[1], ka[2], t * 1e-3, peak_tf) if ka else {}
+            cold[kname] = {"cold_ms_per_launch": round(t, 4), **{k: r[k] for k in ("achieved", "unit", "frac")
+                                                                 if k in r}}
+        out["cold"] = cold
+        out["cold_protocol"] = (f"before each of {cold_steps} steps, outside the timed calls: write "
+                                f"{FLUSH_BYTES >> 20} MiB, then read another {FLUSH_BYTES >> 20} MiB")
+        del fw, fr
+
+    if cpu:
+        host = {n: v for n, v in inp.items()}
+        for n in ("x", "dy", "Wg", "bg", "alive"):
+            host[n] = inp[n].cpu()
+        out["cpu_baseline"] = cpu_baselines(wl, host, counts)
+    del inp, L, calls, step
+    return out
+
+
+def workload_config(wl, recompute=False, sgd=False, alive_topk=False):
+    block = wl.expert == "ffblock"
+    return {"workload": wl.name, "tokens": wl.T, "d_model": wl.D, "expert_hidden": wl.H,
+            "grid": f"{'x'.join([str(wl.M)] * wl.d)}", "experts": wl.N, "k": wl.k,
+            "act": wl.act, "p_alive": wl.p_alive, "pass": "fwd+bwd" if wl.backward else "fwd",
+            "activations": "recomputed in backward" if recompute else "stored",
+            "expert_update": "fused SGD in the backward" if sgd else "gradients returned",
+            "topk": "among alive experts" if alive_topk else "all experts, dead ones weighted 0",
+            "expert": ("Linear-LayerNorm-act-Linear-LayerNorm-act-Linear" if block else "Linear-act-Linear")}
+
+
+def summary(r, steps):
+    """The measurements of an extra workload, for the "workloads" key."""
+    wl = r["wl"]
+    rows = int(sum(r["counts"]))
+    out = {"config": workload_config(wl), "dtype": wl.dtype, "steps": steps,
+           "ms_per_step": round(r["wall"] * 1e3 / steps, 3),
+           "tokens_per_s": round(wl.T * steps / r["wall"], 1),
+           "step_device_ms_median": round(r["per_step"][len(r["per_step"]) // 2], 4),
+           "calls_ms": {n: round(v, 4) for n, v in r["ms"].items()},
+           "calls_roofline": {n: {k: v[k] for k in ("bound", "achieved", "unit", "frac")}
+                              for n, v in r["call_roofline"].items()},
+           "rows_used": rows, "max_rows_per_expert": int(max(r["counts"])),
+           "experts_without_rows": int(sum(1 for c in r["counts"] if c == 0)),
+           "top_kernels": r["kernels"][:6]}
+    if wl.name == "tiny_f32":
+        out["step_device_us_median"] = round(r["per_step"][len(r["per_step"]) // 2] * 1e3, 1)
+    if "cold" in r:
+        out["cold"] = r["cold"]
+        out["cold_protocol"] = r["cold_protocol"]
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="wide")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="time only --workload (no other workloads)")
+    ap.add_argument("--cold-steps", type=int, default=5)
     ap.add_argument("--recompute", action="store_true",
                     help="backward regenerates h and a (dmoe_expert_ffn_bwd_recompute)")
     ap.add_argument("--alive-topk", action="store_true",
@@ -200,157 +512,76 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2002_04013_amd import DMoEBlockLayer, DMoELayer
-    from workloads import (get_workload, make_alive, make_block_experts, make_dy, make_experts, make_gate,
-                           make_x)
+    from workloads import get_workload
 
     wl = get_workload(args.workload)
-    block = wl.expert == "ffblock"
-    if block and (args.recompute or args.sgd):
+    if wl.expert == "ffblock" and (args.recompute or args.sgd):
         print("bench.py: --recompute and --sgd apply to the Linear-act-Linear experts only", file=sys.stderr)
         sys.exit(2)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    t_gen = time.perf_counter()
-    Wg, bg = make_gate(wl, dev)
-    inp = dict(x=make_x(wl, dev), dy=make_dy(wl, dev), Wg=Wg, bg=bg, alive=make_alive(wl, dev))
-    dWg, dbg = torch.empty_like(Wg), torch.empty_like(bg)
-    from paper_2002_04013_amd.abi import DMOE_FLAG_ALIVE_TOPK
-    flags = DMOE_FLAG_ALIVE_TOPK if args.alive_topk else 0
-    if block:
-        prm = make_block_experts(wl, dev)
-        inp["params"] = prm
-        grads = {n: torch.empty_like(v) for n, v in prm.items()}
-        L = DMoEBlockLayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, flags=flags)
+    torch.cuda.set_device(0)
+    modes = dict(recompute=args.recompute, sgd=args.sgd, alive_topk=args.alive_topk)
+    r = run_workload(args.workload, args.steps, args.warmup,
+                     cold_steps=args.cold_steps if args.workload in COLD_WORKLOADS else 0,
+                     cpu=not args.no_cpu_baseline, **modes)
+    ms, kernels, peak_tf = r["ms"], r["kernels"], r["peak_tf"]
+
+    # the roofline object: the kernel that takes the most device time per step
+    dom = kernels[0]
+    if "frac" in dom:
+        roofline = {k: dom[k] for k in ("bound", "achieved", "peak", "unit", "frac")}
     else:
-        W1, b1, W2, b2 = make_experts(wl, dev)
-        inp.update(W1=W1, b1=b1, W2=W2, b2=b2)
-        dW1, db1 = torch.empty_like(W1), torch.empty_like(b1)
-        dW2, db2 = torch.empty_like(W2), torch.empty_like(b2)
-        L = DMoELayer(wl.T, wl.D, wl.H, wl.d, wl.M, wl.k, wl.dtype, wl.act, device=dev, dh_aliases_h=False,
-                      flags=flags)
-    torch.cuda.synchronize()
-    print(f"[bench] {wl.name}: inputs ready in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr,
-          flush=True)
-
-    x, alive = inp["x"], inp["alive"]
-    from paper_2002_04013_amd import abi
-    Dm = L.dims
-    stream = torch.cuda.current_stream()
-
-    def step(ev=None):
-        calls = [
-            ("gate_topk", lambda: abi.dmoe_gate_topk(Dm, x, Wg, bg, alive, L.idx, L.w, None, None, L.ws)),
-            ("dispatch", lambda: abi.dmoe_dispatch(Dm, x, L.idx, alive, L.counts, L.offsets, L.row_token,
-                                                   L.pos, L.x_perm, L.ws)),
-            ("ffn_fwd", (lambda: abi.dmoe_expert_ffblock_fwd(Dm, L.offsets, L.x_perm, prm, L.acts, L.y_perm,
-                                                             L.ws)) if block else
-             (lambda: abi.dmoe_expert_ffn_fwd(Dm, L.offsets, L.x_perm, W1, b1, W2, b2, L.h, L.a,
-                                              L.y_perm, L.ws))),
-            ("combine", lambda: abi.dmoe_combine(Dm, L.y_perm, L.pos, L.w, L.y)),
-            ("combine_bwd", lambda: abi.dmoe_combine_bwd(Dm, inp["dy"], L.y_perm, L.pos, L.w, L.dy_perm,
-                                                         L.dw)),
-            ("gate_topk_bwd", lambda: abi.dmoe_gate_topk_bwd(Dm, x, L.idx, L.w, L.dw, alive, L.dg, dWg, dbg,
-                                                             L.ws)),
-            ("ffn_bwd", (lambda: abi.dmoe_expert_ffblock_bwd(Dm, L.offsets, L.x_perm, prm, L.acts, L.dy_perm,
-                                                             L.g1, L.g2, L.dx_perm, grads, L.ws)) if block else
-             (lambda: abi.dmoe_expert_ffn_bwd_sgd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
-                                                             L.dy_perm, W1, b1, W2, b2, 1e-4, L.dh, L.dx_perm,
-                                                             L.ws)) if args.sgd else
-             (lambda: abi.dmoe_expert_ffn_bwd_recompute(Dm, L.offsets, L.counts, L.x_perm, W1, b1, W2,
-                                                        L.dy_perm, L.h, L.a, L.dx_perm, dW1, db1,
-                                                        dW2, db2, L.ws)) if args.recompute else
-             (lambda: abi.dmoe_expert_ffn_bwd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a,
-                                              L.dy_perm, W1, W2, L.dh, L.dx_perm, dW1, db1, dW2,
-                                              db2, L.ws))),
-            ("dispatch_bwd", lambda: abi.dmoe_dispatch_bwd(Dm, L.dx_perm, L.pos, L.idx, L.dg, Wg, L.dx)),
-        ]
-        for name, fn in calls:
-            if not wl.backward and name not in FWD_CALLS:
-                continue
-            if ev is not None:
-                ev[name][0].record(stream)
-            fn()
-            if ev is not None:
-                ev[name][1].record(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    counts = L.counts.cpu().tolist()
-
-    timed = [n for n in CALLS if wl.backward or n in FWD_CALLS]
-    evs = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in timed}
-           for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(evs[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in evs) / args.steps for n in timed}
-    # per-step device time (first call's start to last call's end event of each step)
-    per_step = sorted(e[timed[0]][0].elapsed_time(e[timed[-1]][1]) for e in evs)
-    print(f"[bench] {args.steps} steps in {wall:.3f} s; per call ms: " +
-          ", ".join(f"{n} {v:.3f}" for n, v in ms.items()), file=sys.stderr, flush=True)
-
-    alg = algorithmic(wl, counts, args.recompute, args.sgd)
-    if block:
-        alg.update(algorithmic_block(wl, counts))
-    peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
-    ridge = peak_tf * 1e12 / (PEAK_HBM_GBS * 1e9)
-
-    def roof(name):
-        a = alg[name]
-        t = ms[name] * 1e-3
-        ai = a["flops"] / max(a["bytes"], 1)
-        if a["flops"] and ai >= ridge:
-            ach = a["flops"] / t / 1e12
-            return {"bound": "mfma", "achieved": round(ach, 1), "peak": peak_tf, "unit": "TFLOP/s",
-                    "frac": round(ach / peak_tf, 4)}
-        ach = a["bytes"] / t / 1e9
-        return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(ach / PEAK_HBM_GBS, 4)}
-
-    kern = ("grouped_gemm2 x3 + ln_act_fwd_kernel x2 (dmoe_expert_ffblock_fwd)" if block else
-            "grouped_gemm2 (dmoe_expert_ffn_fwd: up- and down-projection launches + 1-block tile plan)")
-    roofline = dict(roof("ffn_fwd"), kernel=kern, traffic=measured_traffic(wl.name),
-                    per_launch={"flops": alg["ffn_fwd"]["flops"], "bytes": alg["ffn_fwd"]["bytes"],
-                                "ms": round(ms["ffn_fwd"], 4)})
+        roofline = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None}
+    roofline.update(kernel=dom["name"], role=dom.get("role"), launches_per_step=dom["launches_per_step"],
+                    ms_per_launch=dom["ms_per_launch"], flops_per_launch=dom.get("flops_per_launch"),
+                    bytes_per_launch=dom.get("bytes_per_launch"),
+                    traffic=measured_traffic(wl.name, dom["name"]),
+                    timing="HIP events on the launch stream around every kernel of the timed steps")
     result = {
         "metric": METRIC,
-        "value": round(wl.T * args.steps / wall, 1),
+        "value": round(wl.T * args.steps / r["wall"], 1),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(wall * 1e3 / args.steps, 3),
+        "ms_per_step": round(r["wall"] * 1e3 / args.steps, 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic (seeded N(0,1) inputs, N(0,1/fan_in) weights, random init)",
-        "config": {"workload": wl.name, "tokens": wl.T, "d_model": wl.D, "expert_hidden": wl.H,
-                   "grid": f"{'x'.join([str(wl.M)] * wl.d)}", "experts": wl.N, "k": wl.k,
-                   "act": wl.act, "p_alive": wl.p_alive, "pass": "fwd+bwd" if wl.backward else "fwd",
-                   "activations": "recomputed in backward" if args.recompute else "stored",
-                   "expert_update": "fused SGD in the backward" if args.sgd else "gradients returned",
-                   "topk": "among alive experts" if args.alive_topk else "all experts, dead ones weighted 0",
-                   "expert": ("Linear-LayerNorm-act-Linear-LayerNorm-act-Linear" if block else
-                              "Linear-act-Linear")},
+        "config": workload_config(wl, **modes),
         "roofline": roofline,
-        "roofline_ffn_bwd": roof("ffn_bwd") if wl.backward else None,
-        "gate_topk": roof("gate_topk"),
-        "dispatch": roof("dispatch"),
+        "kernels": kernels,
+        "roofline_ffn_fwd": r["call_roofline"]["ffn_fwd"],
+        "roofline_ffn_bwd": r["call_roofline"].get("ffn_bwd"),
+        "gate_topk": r["call_roofline"]["gate_topk"],
+        "dispatch": r["call_roofline"]["dispatch"],
         "calls_ms": {n: round(v, 4) for n, v in ms.items()},
-        "step_ms": {"median": round(per_step[len(per_step) // 2], 3), "min": round(per_step[0], 3),
-                    "max": round(per_step[-1], 3)},
+        "step_ms": {"median": round(r["per_step"][len(r["per_step"]) // 2], 3), "min": round(r["per_step"][0], 3),
+                    "max": round(r["per_step"][-1], 3)},
+        "paper_context": PAPER_CONTEXT,
     }
-    if not args.no_cpu_baseline:
-        host = {n: v for n, v in inp.items()}
-        for n in ("x", "dy", "Wg", "bg", "alive"):
-            host[n] = inp[n].cpu()
-        result["cpu_baseline"] = cpu_baseline(wl, host, counts)
+    if "cold" in r:
+        result["gate_dispatch_cold"] = r["cold"]
+        result["cold_protocol"] = r["cold_protocol"]
+    if "cpu_baseline" in r:
+        result["cpu_baseline"] = r["cpu_baseline"]
+    del r
+    gc.collect()
+    torch.cuda.empty_cache()
+
+    if not args.no_extra and not any(modes.values()):
+        extra = {}
+        for name in EXTRA_WORKLOADS:
+            if name == args.workload:
+                continue
+            st = 20 if name == "tiny_f32" else 5
+            rr = run_workload(name, st, 2, cold_steps=3 if name in COLD_WORKLOADS else 0)
+            extra[name] = summary(rr, st)
+            del rr
+            gc.collect()
+            torch.cuda.empty_cache()
+        result["workloads"] = extra
     print(json.dumps(result), flush=True)
 
 

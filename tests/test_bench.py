@@ -47,3 +47,25 @@ def test_block_workload_flops():
     # three linear layers D->F, F->F, F->D: 2 P (D F + F F + F D) flops forward
     assert b["ffn_fwd"]["flops"] == 2 * P * (2 * D * F + F * F)
     assert b["ffn_bwd"]["flops"] == 2 * b["ffn_fwd"]["flops"]
+
+
+def test_kernel_rooflines_closed_forms():
+    import bench
+    from workloads import get_workload
+    wl = get_workload("wide")
+    counts = [wl.T * wl.k // wl.N] * wl.N
+    P, D, H, e = wl.T * wl.k, wl.D, wl.H, 2
+    dw = bench.kernel_algorithmic("grouped_gemm2<GM=1,AT=1,BT=1,EPI=0,256x256,ST=2,BK=64>", wl, counts)
+    assert dw[0] == "expert weight-gradient GEMM" and dw[1] == 2 * P * D * H
+    # reads both row operands once and writes every expert's gradient once
+    assert dw[2] == P * (D + H) * e + wl.N * D * H * e
+    up = bench.kernel_algorithmic("grouped_gemm2<GM=0,AT=0,BT=0,EPI=2,256x256,ST=2,BK=64>", wl, counts)
+    assert up[1] == 2 * P * D * H and up[2] == wl.N * (D * H + H) * e + P * (D + 2 * H) * e
+    # the per-launch flops of the five GEMM kinds of one step add up to the call totals
+    names = ["grouped_gemm2<GM=0,AT=0,BT=0,EPI=2", "grouped_gemm2<GM=0,AT=0,BT=0,EPI=1",
+             "grouped_gemm2<GM=0,AT=0,BT=1,EPI=3", "grouped_gemm2<GM=0,AT=0,BT=1,EPI=0"]
+    fl = sum(bench.kernel_algorithmic(n, wl, counts)[1] for n in names) + 2 * dw[1]
+    a = bench.algorithmic(wl, counts)
+    assert fl == a["ffn_fwd"]["flops"] + a["ffn_bwd"]["flops"]
+    r = bench.roofline_of(dw[1], dw[2], 0.02, bench.PEAK_BF16_TFLOPS)
+    assert r["bound"] == "mfma" and abs(r["achieved"] - dw[1] / 0.02 / 1e12) < 0.1
