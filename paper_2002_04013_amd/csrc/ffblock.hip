@@ -324,7 +324,7 @@ static void ln_bwd(const Shape& s, const int32_t* offsets, const E* h, const flo
 template <typename E, typename C>
 static void lin_fwd(const Shape& s, const int32_t* offsets, const int32_t* tpre, const E* A, int n_in,
                     const E* W, const E* b, int n_out, E* Cp, hipStream_t st) {
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
   const int nt = (n_out + C::BN - 1) / C::BN;
   GemmArgs<E> p = args_m<E>(offsets, tpre, nt, (int)s.N);
   p.A = A; p.lda = n_in;
@@ -333,7 +333,7 @@ static void lin_fwd(const Shape& s, const int32_t* offsets, const int32_t* tpre,
   p.bias = b; p.bias_gstride = n_out;
   p.N = n_out; p.K = n_in; p.act = s.act;
   if constexpr (sizeof(E) == 2)
-    run_gemm2<GROUP_M, false, false, EPI_BIAS, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, false, EPI_BIAS, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
   else
     run_gemm<E, GROUP_M, true, EPI_BIAS, C::BM, C::BN, C::BK, C::WM, C::WN>(p, mt_ub * nt, st);
 }
@@ -342,7 +342,7 @@ static void lin_fwd(const Shape& s, const int32_t* offsets, const int32_t* tpre,
 template <typename E, typename C>
 static void lin_dgrad(const Shape& s, const int32_t* offsets, const int32_t* tpre, const E* dC, int n_out,
                       const E* W, int n_in, E* dA, hipStream_t st) {
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
   const int nt = (n_in + C::BN - 1) / C::BN;
   GemmArgs<E> p = args_m<E>(offsets, tpre, nt, (int)s.N);
   p.A = dC; p.lda = n_out;
@@ -350,7 +350,7 @@ static void lin_dgrad(const Shape& s, const int32_t* offsets, const int32_t* tpr
   p.C = dA; p.ldc = n_in;
   p.N = n_in; p.K = n_out; p.act = s.act;
   if constexpr (sizeof(E) == 2)
-    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
   else
     run_gemm<E, GROUP_M, false, EPI_STORE, C::BM, C::BN, C::BK, C::WM, C::WN>(p, mt_ub * nt, st);
 }
@@ -394,7 +394,7 @@ template <typename E, typename C>
 static void block_fwd(const Shape& s, const int32_t* offsets, const E* xp, const BlockP<E>& q, const BlockA<E>& t,
                       E* yp, int32_t* tpre, hipStream_t st) {
   const int D = (int)s.D, F = (int)s.H;
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, (int)s.N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, (int)s.N, C::TMR, tpre);
   lin_fwd<E, C>(s, offsets, tpre, xp, D, q.W1, q.b1, F, t.h1, st);
   ln_fwd<E>(s, offsets, t.h1, q.g1, q.be1, t.a1, t.st1, st);
   lin_fwd<E, C>(s, offsets, tpre, t.a1, F, q.W2, q.b2, F, t.h2, st);
@@ -408,7 +408,7 @@ static void block_bwd(const Shape& s, const int32_t* offsets, const E* xp, const
                       const E* dyp, E* g1, E* g2, E* dxp, const BlockG<E>& d, int32_t* tpre, hipStream_t st) {
   const int D = (int)s.D, F = (int)s.H;
   const int32_t* tact = tpre + s.N + 1;
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, (int)s.N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, (int)s.N, C::TMR, tpre);
   lin_wgrad<E, CW>(s, offsets, tact, dyp, D, t.a2, F, d.W3, st);     // dW3 = dy^T a2
   colsum<E>(s, offsets, dyp, D, d.b3, st);                            // db3
   lin_dgrad<E, C>(s, offsets, tpre, dyp, D, q.W3, F, g2, st);        // da2 = dy W3

@@ -11,8 +11,8 @@ static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
                          const bf16* b1, const bf16* W2, const bf16* b2, bf16* h, bf16* a, bf16* yp,
                          int32_t* tpre, hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::TMR, tpre);
   {
     const int nt = (H + C::BN - 1) / C::BN;
     GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
@@ -21,7 +21,7 @@ static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.C = h; p.ldc = H; p.C2 = a;
     p.bias = b1; p.bias_gstride = H;
     p.N = H; p.K = D; p.act = s.act;
-    run_gemm2<GROUP_M, false, false, EPI_BIAS_ACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, false, EPI_BIAS_ACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
   }
   {
     const int nt = (D + C::BN - 1) / C::BN;
@@ -31,7 +31,7 @@ static void ffn_fwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.C = yp; p.ldc = D;
     p.bias = b2; p.bias_gstride = D;
     p.N = D; p.K = H; p.act = s.act;
-    run_gemm2<GROUP_M, false, false, EPI_BIAS, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, false, EPI_BIAS, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
   }
 }
 
@@ -41,8 +41,8 @@ template <typename C>
 static void ffn_up_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, const bf16* W1, const bf16* b1,
                         bf16* h, bf16* a, int32_t* tpre, hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::TMR, tpre);
   const int nt = (H + C::BN - 1) / C::BN;
   GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
   p.A = xp; p.lda = D;
@@ -50,7 +50,7 @@ static void ffn_up_bf16(const Shape& s, const int32_t* offsets, const bf16* xp, 
   p.C = h; p.ldc = H; p.C2 = a;
   p.bias = b1; p.bias_gstride = H;
   p.N = H; p.K = D; p.act = s.act;
-  run_gemm2<GROUP_M, false, false, EPI_BIAS_ACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+  run_gemm2<GROUP_M, false, false, EPI_BIAS_ACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
 }
 
 template <typename C, typename CW>
@@ -58,10 +58,10 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
                          const bf16* a, const bf16* dyp, const bf16* W1, const bf16* W2, bf16* dh, bf16* dxp,
                          bf16* dW1, bf16* db1, bf16* dW2, bf16* db2, int32_t* tpre, hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
   const int64_t active_ub = std::min<int64_t>(s.N, s.P);
   const int32_t* tact = tpre + N + 1;
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::TMR, tpre);
   {   // dh = (dy W2) * act'(h): W2_e read as (n = h, k = d), N-contiguous
     const int nt = (H + C::BN - 1) / C::BN;
     GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
@@ -69,7 +69,7 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
     p.C = dh; p.ldc = H; p.aux = h;
     p.N = H; p.K = D; p.act = s.act;
-    run_gemm2<GROUP_M, false, true, EPI_DACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, true, EPI_DACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
   }
   {   // dW2_e = dy_e^T a_e   [D, H]
     const int mt = (D + CW::BM - 1) / CW::BM, nt = (H + CW::BN - 1) / CW::BN;
@@ -87,7 +87,7 @@ static void ffn_bwd_bf16(const Shape& s, const int32_t* offsets, const bf16* xp,
     p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
     p.C = dxp; p.ldc = D;
     p.N = D; p.K = H; p.act = s.act;
-    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
   }
   {   // dW1_e = dh_e^T x_e   [H, D]
     const int mt = (H + CW::BM - 1) / CW::BM, nt = (D + CW::BN - 1) / CW::BN;
@@ -112,10 +112,10 @@ static void ffn_bwd_sgd_bf16(const Shape& s, const int32_t* offsets, const bf16*
                              const bf16* dyp, bf16* W1, bf16* b1, bf16* W2, bf16* b2, float lr, const bf16* h,
                              bf16* dh, bf16* dxp, int32_t* tpre, hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
   const int64_t active_ub = std::min<int64_t>(s.N, s.P);
   const int32_t* tact = tpre + N + 1;
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::TMR, tpre);
   {   // dh = (dy W2) * act'(h)
     const int nt = (H + C::BN - 1) / C::BN;
     GemmArgs<bf16> p = args_m<bf16>(offsets, tpre, nt, N);
@@ -123,7 +123,7 @@ static void ffn_bwd_sgd_bf16(const Shape& s, const int32_t* offsets, const bf16*
     p.B = W2; p.ldb = H; p.b_gstride = (int64_t)D * H;
     p.C = dh; p.ldc = H; p.aux = h;
     p.N = H; p.K = D; p.act = s.act;
-    run_gemm2<GROUP_M, false, true, EPI_DACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, true, EPI_DACT, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
   }
   {   // W2_e -= lr dy_e^T a_e
     const int mt = (D + CW::BM - 1) / CW::BM, nt = (H + CW::BN - 1) / CW::BN;
@@ -141,7 +141,7 @@ static void ffn_bwd_sgd_bf16(const Shape& s, const int32_t* offsets, const bf16*
     p.B = W1; p.ldb = D; p.b_gstride = (int64_t)H * D;
     p.C = dxp; p.ldc = D;
     p.N = D; p.K = H; p.act = s.act;
-    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK>(p, mt_ub * nt, st);
+    run_gemm2<GROUP_M, false, true, EPI_STORE, C::BM, C::BN, C::WM, C::WN, C::ST, C::BK, STORE_DIRECT, C::XB>(p, mt_ub * nt, st);
   }
   {   // W1_e -= lr dh_e^T x_e
     const int mt = (H + CW::BM - 1) / CW::BM, nt = (D + CW::BN - 1) / CW::BN;
@@ -163,8 +163,8 @@ static void ffn_fwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
                         const E* b1, const E* W2, const E* b2, E* h, E* a, E* yp, int32_t* tpre,
                         hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::TMR, tpre);
   // h = x W1^T + b1, a = act(h)
   {
     const int nt = (H + C::BN - 1) / C::BN;
@@ -198,10 +198,10 @@ static void ffn_bwd_cfg(const Shape& s, const int32_t* offsets, const E* xp, con
                         E* db1, E* dW2, E* db2, int32_t* tpre, hipStream_t st, float lr = 0.f) {
   constexpr int EPI_W = SGD ? EPI_SGD : EPI_STORE;
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
   const int64_t active_ub = std::min<int64_t>(s.N, s.P);
   const int32_t* tact = tpre + N + 1;
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::TMR, tpre);
   // dh = (dy W2) * act'(h)       B = W2_e viewed as (n = h, k = d): N-contiguous
   {
     const int nt = (H + C::BN - 1) / C::BN;
@@ -254,8 +254,8 @@ template <typename E, typename C>
 static void ffn_up_cfg(const Shape& s, const int32_t* offsets, const E* xp, const E* W1, const E* b1, E* h, E* a,
                        int32_t* tpre, hipStream_t st) {
   const int N = (int)s.N, D = (int)s.D, H = (int)s.H;
-  const int64_t mt_ub = (s.P + C::BM - 1) / C::BM + std::min<int64_t>(s.N, s.P);
-  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::BM, tpre);
+  const int64_t mt_ub = (s.P + C::TMR - 1) / C::TMR + std::min<int64_t>(s.N, s.P);
+  DMOE_LAUNCH(tile_plan, dim3(1), dim3(1024), 0, st, offsets, N, C::TMR, tpre);
   const int nt = (H + C::BN - 1) / C::BN;
   GemmArgs<E> p = args_m<E>(offsets, tpre, nt, N);
   p.A = xp; p.lda = D;

@@ -110,6 +110,16 @@ struct KcTile {
     const int c = (kc + (lane >> 5)) ^ swz_kc<BK, SW>(r);
     return *reinterpret_cast<const bf16x8_t*>(lds + r * RB + c * 16);
   }
+  // The same fragment split into a per-lane part and a per-fragment constant: the
+  // swizzle repeats every 16 rows, so for r0 a multiple of 16 the byte offset is
+  // r0 * RB + lane_off(kc, lane), the second term the same for every r0.
+  __device__ __forceinline__ static uint32_t lane_off(int kc, int lane) {
+    const int r = lane & 31;
+    return (uint32_t)(r * RB + (((kc + (lane >> 5)) ^ swz_kc<BK, SW>(r)) << 4));
+  }
+  __device__ __forceinline__ static bf16x8_t frag_at(const char* lds, int r0, uint32_t off) {
+    return *reinterpret_cast<const bf16x8_t*>(lds + r0 * RB + off);
+  }
 };
 
 // ---- N-contiguous tile [BK][R] (row = k) ---------------------------------------------
@@ -162,6 +172,24 @@ struct NcTile {
       const char* a = lds + k * (R * 2) + ((chunk ^ swz(k)) << 4) + within;
       hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t*)(a));
     }
+    typedef short s16x8_t __attribute__((ext_vector_type(8)));
+    s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8_t, v);
+  }
+  // The same fragment for columns 32 m .. 32 m + 31 split into a per-lane part and a
+  // k-dependent constant: kk a multiple of 16 leaves the swizzle 4 (k % 4) unchanged,
+  // so the lower read is at kk * 2R + lane_off(m, lane) and the upper one 4 rows on.
+  __device__ __forceinline__ static uint32_t lane_off(int m, int lane) {
+    const int g = lane >> 4, i = lane & 15;
+    const int col = 32 * m + 16 * (g & 1) + 4 * (i & 3);
+    const int k = 8 * (g >> 1) + (i >> 2);
+    return (uint32_t)(k * (R * 2) + (((col >> 3) ^ swz(k)) << 4) + (col & 7) * 2);
+  }
+  __device__ __forceinline__ static bf16x8_t frag_at(const char* lds, int kk, uint32_t off) {
+    const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4_t*)(lds + kk * (R * 2) + off));
+    const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4_t*)(lds + (kk + 4) * (R * 2) + off));
     typedef short s16x8_t __attribute__((ext_vector_type(8)));
     s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     return __builtin_bit_cast(bf16x8_t, v);
@@ -231,8 +259,15 @@ __device__ __forceinline__ int stg_off(int r, int c) { return r * 128 + ((c ^ ((
 // as its block j = b / WM, so a partly filled tile (the last m-tile of an expert)
 // spreads its live blocks over all wave rows and SIMDs.  Each wave runs a loop
 // specialised for its number of live blocks, so the loop body has no branches.
+//
+// Extra block (XB = 1, GROUP_M with 256 x 256 tiles of 8 waves): a tile holds up to
+// 288 rows, the 32 beyond the first 256 forming a ninth row block that all 8 waves
+// share, wave (wm, wn) computing its 32 x 32 piece at the wave's own column block wm.
+// An expert's rows are then split into ceil(rows / 288) tiles of equal block counts, so
+// an expert with a few rows more than a multiple of 256 gets no nearly empty tile
+// (which would stream the expert's whole weight slab again for those rows).
 template <int GM, bool A_T, bool B_T, int EPI, int BM, int BN, int WM, int WN, int STAGES, int SW, int BK,
-          int STO = STORE_DIRECT>
+          int STO = STORE_DIRECT, int XB = 0>
 __global__ void __launch_bounds__(64 * WM * WN)
 grouped_gemm2(GemmArgs<bf16> p) {
   constexpr int NW = WM * WN, NT = 64 * NW;
@@ -241,15 +276,21 @@ grouped_gemm2(GemmArgs<bf16> p) {
   constexpr int KK = BK / 16;
   using TA = typename std::conditional<A_T, NcTile<BM, NW, BK>, KcTile<BM, NW, SW, BK>>::type;
   using TB = typename std::conditional<B_T, NcTile<BN, NW, BK>, KcTile<BN, NW, SW, BK>>::type;
-  constexpr int ABYTES = TA::BYTES, SBYTES = TA::BYTES + TB::BYTES;
+  constexpr int XROWS = XB ? 32 : 0;                 // rows of the extra block
+  constexpr int BMT = BM + XROWS;                    // rows a tile can hold
+  constexpr int ABYTES = TA::BYTES + XROWS * BK * 2, SBYTES = ABYTES + TB::BYTES;
   constexpr int LPS = TA::PER_WAVE + TB::PER_WAVE;   // load instructions per stage per wave
+  // (with XB, waves 0..3 load one more: the extra block's 32 rows, 8 rows each)
   // store instructions of a full tile's epilogue, per wave
   constexpr int SFULL = EPI == EPI_F32 ? TM * TN * 4 : TM * TN * 2 * (EPI == EPI_BIAS_ACT ? 2 : 1);
   static_assert(TM >= 1 && TM <= 5 && TN >= 1, "tile");
   // GROUP_M tiles taller than 256 rows split each expert's rows evenly (in 32-row
   // blocks) over its m-tiles, so an expert slightly above a multiple of the tile height
   // gets no nearly empty last tile
-  constexpr bool BAL = GM == GROUP_M && BM > 256;
+  constexpr bool BAL = GM == GROUP_M && (BM > 256 || XB);
+  static_assert(!XB || (GM == GROUP_M && !A_T && BM == 256 && BN == 256 && WM == 4 && WN == 2 && STAGES == 2 &&
+                        STO == STORE_DIRECT && EPI != EPI_F32 && EPI != EPI_SGD),
+                "extra block: GROUP_M 256 x 256 tiles of 8 waves, 2 stages, direct stores");
   static_assert(KK % 2 == 0, "fragment slots alternate over an even number of steps");
   static_assert(TA::INSTR % NW == 0 && TB::INSTR % NW == 0, "equal load counts per wave");
   static_assert(GM == GROUP_M || (A_T && B_T), "GROUP_K takes both operands stored per token");
@@ -261,6 +302,22 @@ grouped_gemm2(GemmArgs<bf16> p) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
+  const int lps = LPS + (XB && wave < 4 ? 1 : 0);     // this wave's loads per stage
+  // per-lane byte offsets of the MFMA fragments within a stage: K-contiguous tiles by
+  // k-step (shared by A and B, whose rows have the same width and swizzle), N-contiguous
+  // tiles by 32-column block
+  uint32_t kc_off[KK], a_nc[TM], b_nc[TN], bx_nc = 0;
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) kc_off[kk] = KcTile<BM, NW, SW, BK>::lane_off(kk * 2, lane);
+  if constexpr (A_T) {
+#pragma unroll
+    for (int j = 0; j < TM; ++j) a_nc[j] = TA::lane_off(j * WM + wm, lane);
+  }
+  if constexpr (B_T) {
+#pragma unroll
+    for (int i = 0; i < TN; ++i) b_nc[i] = TB::lane_off(wn * TN + i, lane);
+    if constexpr (XB) bx_nc = TB::lane_off(wn * TN + wm, lane);
+  }
 
   const int total = ld_plan(p.tprefix, p.groups) * p.tscale;
   int L, Lend, Lstep;
@@ -301,11 +358,14 @@ grouped_gemm2(GemmArgs<bf16> p) {
     t.off = ld_plan(p.offsets, t.e);
     const int cnt = ld_plan(p.offsets, t.e + 1) - t.off;
     if constexpr (GM == GROUP_M) {
-      const int mt_e = (cnt + BM - 1) / BM;
+      const int mt_e = (cnt + BMT - 1) / BMT;
       if constexpr (BAL) {
-        const int bpt = ((cnt + 31) / 32 + mt_e - 1) / mt_e;   // 32-row blocks per m-tile
-        t.m0 = (q % mt_e) * bpt * 32;
-        t.mvalid = cnt - t.m0 < bpt * 32 ? cnt - t.m0 : bpt * 32;
+        // m-tile qm holds 32-row blocks [qm B / mt_e, (qm + 1) B / mt_e) of the expert's
+        // B blocks: tile sizes differ by at most one block
+        const int nb = (cnt + 31) / 32, qm = q % mt_e;
+        const int b0 = qm * nb / mt_e, b1 = (qm + 1) * nb / mt_e;
+        t.m0 = b0 * 32;
+        t.mvalid = cnt - t.m0 < (b1 - b0) * 32 ? cnt - t.m0 : (b1 - b0) * 32;
       } else {
         t.m0 = (q % mt_e) * BM;
         t.mvalid = cnt - t.m0;
@@ -337,6 +397,17 @@ grouped_gemm2(GemmArgs<bf16> p) {
     const int k0 = kt * BK;
     if constexpr (A_T) TA::load(t.Ab + (int64_t)k0 * p.lda, p.lda, t.mvalid, t.kvalid - k0, buf, wave, lane);
     else TA::load(t.Ab + k0, p.lda, t.mvalid, buf, wave, lane);
+    if constexpr (XB) {
+      // rows BM .. BM+31 of the tile: wave w < 4 loads rows BM + 8w .. BM + 8w + 7
+      if (wave < 4) {
+        constexpr int CH = BK / 8;
+        const int r = BM + wave * (1024 / (BK * 2)) + lane / CH;
+        const int c = (lane % CH) ^ swz_kc<BK, SW>(r);
+        const int rr = r < t.mvalid ? r : t.mvalid - 1;
+        g2l_16_at<0>(t.Ab + k0, ((uint32_t)rr * (uint32_t)p.lda + (uint32_t)(c * 8)) * 2u,
+                     buf + TA::BYTES + wave * 1024);
+      }
+    }
     if constexpr (B_T) TB::load(t.Bb + (int64_t)k0 * p.ldb, p.ldb, t.nvalid, t.kvalid - k0, buf + ABYTES, wave, lane);
     else TB::load(t.Bb + k0, p.ldb, t.nvalid, buf + ABYTES, wave, lane);
   };
@@ -346,7 +417,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
       if (s < t.nk) issue(t, s);
   };
   // stage s of tile t has landed in this wave's view; `after` = load stages issued after it
-  auto wait_stage = [&](int after, int extra) { wait_vmcnt_rt(after * LPS + extra > 63 ? 63 : after * LPS + extra); };
+  auto wait_stage = [&](int after, int extra) { wait_vmcnt_rt(after * lps + extra > 63 ? 63 : after * lps + extra); };
   // GROUP_K: zero the k rows of stage s past the expert's tokens, once every wave's loads landed
   auto fix_tail = [&](const TileC& t, int s) {
     if constexpr (GM == GROUP_K) {
@@ -372,7 +443,9 @@ grouped_gemm2(GemmArgs<bf16> p) {
     const int nk = t.nk;
     const bool more = L + Lstep < Lend;
     int early = 0;                 // stages of the next tile issued before this tile's MFMAs
-    const int nblk = (mvalid + 31) / 32;                 // live 32-row blocks of the tile
+    const int nblk_all = (mvalid + 31) / 32;             // live 32-row blocks of the tile
+    const int nblk = nblk_all < BM / 32 ? nblk_all : BM / 32;
+    const bool xl = XB && nblk_all > BM / 32;            // the extra block is live
     int nl = (nblk - wm + WM - 1) / WM;                  // of them, this wave's (a prefix of j)
     nl = nl < 0 ? 0 : (nl > TM ? TM : nl);
 
@@ -383,25 +456,34 @@ grouped_gemm2(GemmArgs<bf16> p) {
       for (int j = 0; j < TM; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    f32x16_t accx;                                       // the extra block's piece
+#pragma unroll
+    for (int r = 0; r < 16; ++r) accx[r] = 0.f;
 
-    auto mainloop = [&](auto NLc) {
+    auto mainloop = [&](auto NLc, auto XLc) {
       constexpr int NL = decltype(NLc)::value;
-      constexpr int NDS = (A_T ? 2 : 1) * NL + (B_T ? 2 : 1) * TN;   // LDS reads per step
-      bf16x8_t fa[2][TM], fb[2][TN];
+      constexpr bool XL = decltype(XLc)::value;
+      constexpr int NDS = (A_T ? 2 : 1) * NL + (B_T ? 2 : 1) * TN + (XL ? 1 + (B_T ? 2 : 1) : 0);
+      bf16x8_t fa[2][TM], fb[2][TN], fax[2], fbx[2];
       auto ldfrag = [&](const char* buf, int kk, int slot) {
         if constexpr (NL == 0) return;             // no rows: nothing to multiply
         const char* as = buf;
         const char* bs = buf + ABYTES;
+        if constexpr (XL) {
+          fax[slot] = TA::frag_at(as, BM, kc_off[kk]);
+          if constexpr (B_T) fbx[slot] = TB::frag_at(bs, kk * 16, bx_nc);
+          else fbx[slot] = TB::frag_at(bs, wn * WTN + wm * 32, kc_off[kk]);
+        }
 #pragma unroll
         for (int j = 0; j < NL; ++j) {
           const int r0 = (j * WM + wm) * 32;
-          if constexpr (A_T) fa[slot][j] = TA::frag(as, r0, kk * 16, lane);
-          else fa[slot][j] = TA::frag(as, r0, kk * 2, lane);
+          if constexpr (A_T) fa[slot][j] = TA::frag_at(as, kk * 16, a_nc[j]);
+          else fa[slot][j] = TA::frag_at(as, r0, kc_off[kk]);
         }
 #pragma unroll
         for (int i = 0; i < TN; ++i) {
-          if constexpr (B_T) fb[slot][i] = TB::frag(bs, wn * WTN + i * 32, kk * 16, lane);
-          else fb[slot][i] = TB::frag(bs, wn * WTN + i * 32, kk * 2, lane);
+          if constexpr (B_T) fb[slot][i] = TB::frag_at(bs, kk * 16, b_nc[i]);
+          else fb[slot][i] = TB::frag_at(bs, wn * WTN + i * 32, kc_off[kk]);
         }
       };
       auto mm = [&](int slot) {
@@ -410,10 +492,11 @@ grouped_gemm2(GemmArgs<bf16> p) {
 #pragma unroll
           for (int i = 0; i < TN; ++i)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][i], fa[slot][j], acc[i][j], 0, 0, 0);
+        if constexpr (XL) accx = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fbx[slot], fax[slot], accx, 0, 0, 0);
       };
       auto interleave = [&]() {
 #pragma unroll
-        for (int q = 0; q < NL * TN; ++q) {
+        for (int q = 0; q < NL * TN + (XL ? 1 : 0); ++q) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // one MFMA
           if (q < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
         }
@@ -477,12 +560,14 @@ grouped_gemm2(GemmArgs<bf16> p) {
         mm(1);
       }
     };
-    if (nl == TM) mainloop(std::integral_constant<int, TM>{});
-    else if (TM >= 2 && nl == 1) mainloop(std::integral_constant<int, 1>{});
-    else if (TM >= 3 && nl == 2) mainloop(std::integral_constant<int, (TM >= 3 ? 2 : 1)>{});
-    else if (TM >= 4 && nl == 3) mainloop(std::integral_constant<int, (TM >= 4 ? 3 : 1)>{});
-    else if (TM >= 5 && nl == 4) mainloop(std::integral_constant<int, (TM >= 5 ? 4 : 1)>{});
-    else mainloop(std::integral_constant<int, 0>{});
+    using NoX = std::integral_constant<bool, false>;
+    if (XB && xl) mainloop(std::integral_constant<int, TM>{}, std::integral_constant<bool, (XB != 0)>{});
+    else if (nl == TM) mainloop(std::integral_constant<int, TM>{}, NoX{});
+    else if (TM >= 2 && nl == 1) mainloop(std::integral_constant<int, 1>{}, NoX{});
+    else if (TM >= 3 && nl == 2) mainloop(std::integral_constant<int, (TM >= 3 ? 2 : 1)>{}, NoX{});
+    else if (TM >= 4 && nl == 3) mainloop(std::integral_constant<int, (TM >= 4 ? 3 : 1)>{}, NoX{});
+    else if (TM >= 5 && nl == 4) mainloop(std::integral_constant<int, (TM >= 5 ? 4 : 1)>{}, NoX{});
+    else mainloop(std::integral_constant<int, 0>{}, NoX{});
 
     block_sync_lds();      // every wave is done with the ring before the next tile's loads
 
@@ -507,6 +592,17 @@ grouped_gemm2(GemmArgs<bf16> p) {
           bias_v[i][g] = *reinterpret_cast<const uint2*>(p.bias + (int64_t)e * p.bias_gstride + n);
         }
     }
+    uint2 bias_x[4];                                     // the extra block's columns
+    if constexpr (XB && HAS_BIAS) {
+      if (xl) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int nl_ = wn * WTN + wm * 32 + 8 * g + 4 * lhi;
+          bias_x[g] = *reinterpret_cast<const uint2*>(p.bias + (int64_t)e * p.bias_gstride + n0 +
+                                                      (nl_ < nvalid ? nl_ : 0));
+        }
+      }
+    }
 
     if (more) {
       if (early == 0) {
@@ -520,8 +616,105 @@ grouped_gemm2(GemmArgs<bf16> p) {
 
     // epilogue (same accumulator layout as grouped_gemm); stores issued by this wave
     // number SFULL exactly when every row and column of its part of the tile is valid
-    const bool full = nl == TM && mvalid >= BM && nvalid >= BN;
-    prev_stores = full ? SFULL : 0;
+    constexpr int SXB = 2 * (EPI == EPI_BIAS_ACT ? 2 : 1);   // stores of the extra block's piece
+    const bool full = nl == TM && mvalid >= (xl ? BMT : BM) && nvalid >= BN;
+    prev_stores = full ? SFULL + (xl ? SXB : 0) : 0;
+
+    // One 32 x 32 block in C's layout, straight from registers: lane (row l32, half lhi)
+    // holds columns cb + 8g + 4 lhi .. +3 of row crow for g = 0..3 (bias bv and the tile
+    // read in C's layout av per column group).
+    auto emit_direct = [&](const f32x16_t& a, int cb, int64_t crow, bool mok, const uint2 (&bv)[4],
+                           const uint2 (&av)[4]) {
+      uint32_t pk[4][2], pa[4][2];      // bf16 pairs of column group g (output, activation)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int nl_ = cb + 8 * g + 4 * lhi;
+        const int n = n0 + nl_;
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = a[4 * g + r];
+        if constexpr (HAS_BIAS) {
+          const uint2 b = bv[g];
+          v[0] += __uint_as_float(b.x << 16); v[1] += __uint_as_float(b.x & 0xffff0000u);
+          v[2] += __uint_as_float(b.y << 16); v[3] += __uint_as_float(b.y & 0xffff0000u);
+        }
+        if constexpr (EPI == EPI_DACT) {
+          const uint2 hv = av[g];
+          v[0] *= act_bwd_fast(__uint_as_float(hv.x << 16), p.act);
+          v[1] *= act_bwd_fast(__uint_as_float(hv.x & 0xffff0000u), p.act);
+          v[2] *= act_bwd_fast(__uint_as_float(hv.y << 16), p.act);
+          v[3] *= act_bwd_fast(__uint_as_float(hv.y & 0xffff0000u), p.act);
+        }
+        if constexpr (EPI == EPI_SGD) {
+          const uint2 wv = av[g];
+          v[0] = __uint_as_float(wv.x << 16) - p.lr * v[0];
+          v[1] = __uint_as_float(wv.x & 0xffff0000u) - p.lr * v[1];
+          v[2] = __uint_as_float(wv.y << 16) - p.lr * v[2];
+          v[3] = __uint_as_float(wv.y & 0xffff0000u) - p.lr * v[3];
+        }
+        if constexpr (EPI == EPI_F32) {
+          if (mok && nl_ < nvalid)
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          pk[g][0] = f2bf2(v[0], v[1]);
+          pk[g][1] = f2bf2(v[2], v[3]);
+          if constexpr (EPI == EPI_BIAS_ACT) {
+            float ac[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) ac[r] = act_fwd_fast(v[r], p.act);
+            pa[g][0] = f2bf2(ac[0], ac[1]);
+            pa[g][1] = f2bf2(ac[2], ac[3]);
+          }
+        }
+      }
+      if constexpr (EPI != EPI_F32) {
+        // Lanes l and l + 32 hold the two 4-column halves of each 8-column group of one
+        // row.  Swapping the upper lanes of group 2h with the lower lanes of group 2h+1
+        // leaves lane l with columns 16h .. 16h+7 and lane l + 32 with 16h+8 .. 16h+15,
+        // so each lane writes 16 contiguous bytes (all lanes take part in the swaps).
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const auto r = __builtin_amdgcn_permlane32_swap(pk[2 * h2][q], pk[2 * h2 + 1][q], false, false);
+            pk[2 * h2][q] = r[0];
+            pk[2 * h2 + 1][q] = r[1];
+            if constexpr (EPI == EPI_BIAS_ACT) {
+              const auto ra = __builtin_amdgcn_permlane32_swap(pa[2 * h2][q], pa[2 * h2 + 1][q], false, false);
+              pa[2 * h2][q] = ra[0];
+              pa[2 * h2 + 1][q] = ra[1];
+            }
+          }
+          const int c = cb + 16 * h2 + 8 * lhi;
+          if (mok && c < nvalid) {
+            *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + crow + n0 + c) =
+                make_uint4(pk[2 * h2][0], pk[2 * h2][1], pk[2 * h2 + 1][0], pk[2 * h2 + 1][1]);
+            if constexpr (EPI == EPI_BIAS_ACT)
+              *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C2) + crow + n0 + c) =
+                  make_uint4(pa[2 * h2][0], pa[2 * h2][1], pa[2 * h2 + 1][0], pa[2 * h2 + 1][1]);
+          }
+        }
+      }
+    };
+
+    if constexpr (XB) {
+      if (xl) {
+        // the extra block's piece: rows BM .. BM+31 of the tile, column block wm
+        const int ml = BM + l32;
+        const bool mok = ml < mvalid;
+        const int cb = wn * WTN + wm * 32;
+        uint2 aux_x[4];
+        if constexpr (HAS_AUX) {
+          const int64_t arow = (int64_t)(off + m0 + (mok ? ml : 0)) * p.ldc;
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int nl_ = cb + 8 * g + 4 * lhi;
+            aux_x[g] = *reinterpret_cast<const uint2*>(p.aux + arow + n0 + (nl_ < nvalid ? nl_ : 0));
+          }
+        }
+        emit_direct(accx, cb, (int64_t)(off + m0 + ml) * p.ldc, mok, bias_x, aux_x);
+      }
+    }
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       const int ml = (j * WM + wm) * 32 + l32;
@@ -629,78 +822,8 @@ grouped_gemm2(GemmArgs<bf16> p) {
         continue;
       }
 #pragma unroll
-      for (int i = 0; i < TN; ++i) {
-        uint32_t pk[4][2], pa[4][2];      // bf16 pairs of column group g (output, activation)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int nl_ = wn * WTN + i * 32 + 8 * g + 4 * lhi;
-          const int n = n0 + nl_;
-          float v[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * g + r];
-          if constexpr (HAS_BIAS) {
-            const uint2 b = bias_v[i][g];
-            v[0] += __uint_as_float(b.x << 16); v[1] += __uint_as_float(b.x & 0xffff0000u);
-            v[2] += __uint_as_float(b.y << 16); v[3] += __uint_as_float(b.y & 0xffff0000u);
-          }
-          if constexpr (EPI == EPI_DACT) {
-            const uint2 hv = aux_v[i][g];
-            v[0] *= act_bwd_fast(__uint_as_float(hv.x << 16), p.act);
-            v[1] *= act_bwd_fast(__uint_as_float(hv.x & 0xffff0000u), p.act);
-            v[2] *= act_bwd_fast(__uint_as_float(hv.y << 16), p.act);
-            v[3] *= act_bwd_fast(__uint_as_float(hv.y & 0xffff0000u), p.act);
-          }
-          if constexpr (EPI == EPI_SGD) {
-            const uint2 wv = aux_v[i][g];
-            v[0] = __uint_as_float(wv.x << 16) - p.lr * v[0];
-            v[1] = __uint_as_float(wv.x & 0xffff0000u) - p.lr * v[1];
-            v[2] = __uint_as_float(wv.y << 16) - p.lr * v[2];
-            v[3] = __uint_as_float(wv.y & 0xffff0000u) - p.lr * v[3];
-          }
-          if constexpr (EPI == EPI_F32) {
-            if (mok && nl_ < nvalid)
-              *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + crow + n) = make_float4(v[0], v[1], v[2], v[3]);
-          } else {
-            pk[g][0] = f2bf2(v[0], v[1]);
-            pk[g][1] = f2bf2(v[2], v[3]);
-            if constexpr (EPI == EPI_BIAS_ACT) {
-              float a[4];
-#pragma unroll
-              for (int r = 0; r < 4; ++r) a[r] = act_fwd_fast(v[r], p.act);
-              pa[g][0] = f2bf2(a[0], a[1]);
-              pa[g][1] = f2bf2(a[2], a[3]);
-            }
-          }
-        }
-        if constexpr (EPI != EPI_F32) {
-          // Lanes l and l + 32 hold the two 4-column halves of each 8-column group of one
-          // row.  Swapping the upper lanes of group 2h with the lower lanes of group 2h+1
-          // leaves lane l with columns 16h .. 16h+7 and lane l + 32 with 16h+8 .. 16h+15,
-          // so each lane writes 16 contiguous bytes (all lanes take part in the swaps).
-#pragma unroll
-          for (int h2 = 0; h2 < 2; ++h2) {
-#pragma unroll
-            for (int q = 0; q < 2; ++q) {
-              const auto r = __builtin_amdgcn_permlane32_swap(pk[2 * h2][q], pk[2 * h2 + 1][q], false, false);
-              pk[2 * h2][q] = r[0];
-              pk[2 * h2 + 1][q] = r[1];
-              if constexpr (EPI == EPI_BIAS_ACT) {
-                const auto ra = __builtin_amdgcn_permlane32_swap(pa[2 * h2][q], pa[2 * h2 + 1][q], false, false);
-                pa[2 * h2][q] = ra[0];
-                pa[2 * h2 + 1][q] = ra[1];
-              }
-            }
-            const int c = wn * WTN + i * 32 + 16 * h2 + 8 * lhi;
-            if (mok && c < nvalid) {
-              *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C) + crow + n0 + c) =
-                  make_uint4(pk[2 * h2][0], pk[2 * h2][1], pk[2 * h2 + 1][0], pk[2 * h2 + 1][1]);
-              if constexpr (EPI == EPI_BIAS_ACT)
-                *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(p.C2) + crow + n0 + c) =
-                    make_uint4(pa[2 * h2][0], pa[2 * h2][1], pa[2 * h2 + 1][0], pa[2 * h2 + 1][1]);
-            }
-          }
-        }
-      }
+      for (int i = 0; i < TN; ++i)
+        emit_direct(acc[i][j], wn * WTN + i * 32, crow, mok, bias_v[HAS_BIAS ? i : 0], aux_v[HAS_AUX ? i : 0]);
     }
     if constexpr (PRE < STAGES) {
       // stages issued after the epilogue: the stores are no longer the newest operations
@@ -714,9 +837,10 @@ grouped_gemm2(GemmArgs<bf16> p) {
   }
 }
 
-template <int BM, int BN, int STAGES, bool A_T, bool B_T, int BK, int NW = 8, int STO = STORE_DIRECT>
+template <int BM, int BN, int STAGES, bool A_T, bool B_T, int BK, int NW = 8, int STO = STORE_DIRECT, int XB = 0>
 constexpr size_t gemm2_lds_bytes() {
-  return (size_t)STAGES * (BM + BN) * BK * 2 + (STO != STORE_DIRECT ? (size_t)NW * STG_WAVE_BYTES : 0);
+  return (size_t)STAGES * (BM + (XB ? 32 : 0) + BN) * BK * 2 +
+         (STO != STORE_DIRECT ? (size_t)NW * STG_WAVE_BYTES : 0);
 }
 
 }  // namespace dmoe

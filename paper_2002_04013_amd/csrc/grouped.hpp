@@ -159,17 +159,18 @@ static void run_gemm(GemmArgs<E> p, int64_t tiles_ub, hipStream_t st) {
 }
 
 // gfx950 bf16 path: direct-to-LDS multi-stage GEMM (gemm2.hpp)
-template <int GM, bool AT, bool BT, int EPI, int BM, int BN, int WM, int WN, int ST, int BK, int STO = STORE_DIRECT>
+template <int GM, bool AT, bool BT, int EPI, int BM, int BN, int WM, int WN, int ST, int BK, int STO = STORE_DIRECT,
+          int XB = 0>
 static void run_gemm2(GemmArgs<bf16> p, int64_t tiles_ub, hipStream_t st) {
   if (tiles_ub <= 0) return;
-  auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1, BK, STO>;
+  auto kern = grouped_gemm2<GM, AT, BT, EPI, BM, BN, WM, WN, ST, 1, BK, STO, XB>;
   constexpr int NT = 64 * WM * WN;
-  const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT, BK, WM * WN, STO>();
+  const size_t lds = gemm2_lds_bytes<BM, BN, ST, AT, BT, BK, WM * WN, STO, XB>();
   static std::atomic<int> per_cu[MAX_DEVICES];
   static const char* name = [] {
     static char b[96];
-    snprintf(b, sizeof b, "grouped_gemm2<GM=%d,AT=%d,BT=%d,EPI=%d,%dx%d,ST=%d,BK=%d>", GM, (int)AT, (int)BT, EPI, BM,
-             BN, ST, BK);
+    snprintf(b, sizeof b, "grouped_gemm2<GM=%d,AT=%d,BT=%d,EPI=%d,%dx%d,ST=%d,BK=%d%s>", GM, (int)AT, (int)BT, EPI,
+             BM + 32 * XB, BN, ST, BK, XB ? ",XB" : "");
     return b;
   }();
   const int nb = blocks_per_cu(per_cu, (const void*)kern, NT, lds);
@@ -186,8 +187,8 @@ static GemmArgs<E> args_m(const int32_t* offsets, const int32_t* tpre, int scale
   return p;
 }
 
-// fp32 tile shapes (register-staged MFMA GEMM of gemm.hpp).
-struct CfgF32    { static constexpr int BM = 32, BN = 64, BK = 32, WM = 1, WN = 2; };
+// fp32 tile shapes (register-staged MFMA GEMM of gemm.hpp).  TMR: rows an m-tile holds.
+struct CfgF32    { static constexpr int BM = 32, BN = 64, BK = 32, WM = 1, WN = 2, TMR = BM; };
 struct CfgDWF32  { static constexpr int BM = 64, BN = 64, BK = 32, WM = 2, WN = 2; };
 
 // bf16 tile shapes of the gemm2 path: many rows per expert -> 256x256 tiles, 8 waves,
@@ -200,8 +201,13 @@ struct CfgDWF32  { static constexpr int BM = 64, BN = 64, BK = 32, WM = 2, WN = 
 // Weight-gradient tiles write their 128 KiB of output through LDS as whole 128-byte
 // lines with the non-temporal hint: the 64 GiB of weight gradients per step then
 // stream past the L2 instead of evicting the GEMM's operands from it.
-struct G2Fat     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64; };
-struct G2Skinny  { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4, BK = 64; };
+// Many rows per expert: the 256-row tiles take a ninth, shared 32-row block (XB), so an
+// m-tile holds up to 288 rows and an expert's rows split evenly over its m-tiles (an
+// expert of 512 + 18 rows gets two tiles of 9 and 8 blocks instead of a third tile of
+// one block that streams the expert's weights once more).
+struct G2Fat     { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64, XB = 1,
+                   TMR = BM + 32 * XB; };
+struct G2Skinny  { static constexpr int BM = 32, BN = 256, WM = 1, WN = 4, ST = 4, BK = 64, XB = 0, TMR = BM; };
 struct G2DW      { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 2, BK = 64,
                    STO = STORE_STAGED_NT; };
 struct G2DWShort { static constexpr int BM = 256, BN = 256, WM = 4, WN = 2, ST = 4, BK = 32,

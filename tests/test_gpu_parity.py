@@ -19,6 +19,11 @@ CASES = {
     # bf16, fat experts (hundreds of rows each): the 256x256-tile GEMM configuration
     "bf16_fat": Workload("bf16_fat", 11, T=2048, D=128, H=256, d=2, M=4, k=2, dtype="bf16",
                          act="gelu", p_alive=0.9),
+    # fat experts of ~540 rows (one grid dimension, top-1): m-tiles of up to 288 rows
+    # split each expert evenly (the ninth, shared 32-row block live), expert hidden size
+    # off the 256-column tile grid
+    "bf16_fat_xb": Workload("bf16_fat_xb", 31, T=4300, D=128, H=192, d=1, M=8, k=1, dtype="bf16",
+                            act="gelu"),
     # 3-D grid, token count off the tile grid, ReLU
     "bf16_grid3d": Workload("bf16_grid3d", 12, T=333, D=128, H=192, d=3, M=3, k=4, dtype="bf16",
                             act="relu", p_alive=0.85),
