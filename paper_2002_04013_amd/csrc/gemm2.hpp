@@ -149,10 +149,10 @@ struct NcTile {
       g2l_16_at<i * NW * 1024>(base, ((uint32_t)kk * (uint32_t)ld + (uint32_t)col) * 2u, lw);
     });
   }
-  // zero rows [kvalid, BK) of the tile (GROUP_K tail)
-  __device__ __forceinline__ static void zero_tail(char* lds, int kvalid, int tid, int nt) {
+  // zero rows [kvalid, kend) of the tile (GROUP_K tail)
+  __device__ __forceinline__ static void zero_tail(char* lds, int kvalid, int kend, int tid, int nt) {
     uint4* p = reinterpret_cast<uint4*>(lds + kvalid * R * 2);
-    const int n = (BK - kvalid) * CPR;
+    const int n = (kend - kvalid) * CPR;
     for (int i = tid; i < n; i += nt) p[i] = make_uint4(0, 0, 0, 0);
   }
   // MFMA fragment for columns c0 .. c0+31 (lane % 32) and k = kk .. kk+15 (lane / 32 picks 8):
@@ -361,8 +361,12 @@ grouped_gemm2(GemmArgs<bf16> p) {
       const int mt_e = (cnt + BMT - 1) / BMT;
       if constexpr (BAL) {
         // m-tile qm holds 32-row blocks [qm B / mt_e, (qm + 1) B / mt_e) of the expert's
-        // B blocks: tile sizes differ by at most one block
-        const int nb = (cnt + 31) / 32, qm = q % mt_e;
+        // B blocks: tile sizes differ by at most one block.  Odd experts number their
+        // m-tiles backwards, so the persistent blocks that take the same m position
+        // expert after expert (tiles are dealt out in a fixed stride) alternate between
+        // the larger and the smaller tiles instead of one group falling steadily behind
+        // the other, which would stop them sharing each weight slab in L2.
+        const int nb = (cnt + 31) / 32, qm = (t.e & 1) ? mt_e - 1 - q % mt_e : q % mt_e;
         const int b0 = qm * nb / mt_e, b1 = (qm + 1) * nb / mt_e;
         t.m0 = b0 * 32;
         t.mvalid = cnt - t.m0 < (b1 - b0) * 32 ? cnt - t.m0 : (b1 - b0) * 32;
@@ -418,15 +422,20 @@ grouped_gemm2(GemmArgs<bf16> p) {
   };
   // stage s of tile t has landed in this wave's view; `after` = load stages issued after it
   auto wait_stage = [&](int after, int extra) { wait_vmcnt_rt(after * lps + extra > 63 ? 63 : after * lps + extra); };
-  // GROUP_K: zero the k rows of stage s past the expert's tokens, once every wave's loads landed
+  // GROUP_K: zero the k rows of stage s past the expert's tokens, once every wave's loads
+  // landed, up to the end of the last 16-deep MFMA step that reads any row of the
+  // expert (the steps past it are not issued)
   auto fix_tail = [&](const TileC& t, int s) {
     if constexpr (GM == GROUP_K) {
       const int kv = t.kvalid - s * BK;
       if (kv < BK) {
+        const int kend = (kv + 15) / 16 * 16;
         char* buf = slot(t, s);
         block_sync_lds();
-        TA::zero_tail(buf, kv, tid, NT);
-        TB::zero_tail(buf + ABYTES, kv, tid, NT);
+        if (kend > kv) {
+          TA::zero_tail(buf, kv, kend, tid, NT);
+          TB::zero_tail(buf + ABYTES, kv, kend, tid, NT);
+        }
       }
     }
   };
@@ -550,14 +559,17 @@ grouped_gemm2(GemmArgs<bf16> p) {
         interleave();
       }
       {
+        // the last stage; with GROUP_K only its MFMA steps that reach a row of the
+        // expert (rows past the last are zero and would add nothing)
         const char* cur = slot(t, nk - 1);
+        const int nkk = GM == GROUP_K ? (t.kvalid - (nk - 1) * BK + 15) / 16 : KK;
 #pragma unroll
         for (int kk = 0; kk + 1 < KK; ++kk) {
-          ldfrag(cur, kk + 1, (kk & 1) ^ 1);
-          mm(kk & 1);
+          if (kk + 1 < nkk) ldfrag(cur, kk + 1, (kk & 1) ^ 1);
+          if (kk < nkk) mm(kk & 1);
           interleave();
         }
-        mm(1);
+        if (KK - 1 < nkk) mm(1);
       }
     };
     using NoX = std::integral_constant<bool, false>;
