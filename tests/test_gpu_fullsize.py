@@ -6,13 +6,19 @@ Inputs are drawn on the GPU (the weights of the large workloads do not fit the
 host) and the oracle reads back what it needs.  Checked against the oracle:
   * every token: gate scores (within one fp32 ulp of exact), TopK indices and
     order (bit-exact), Eq. 1 weights, and the whole dispatch (bit-exact);
-  * sampled experts (the busiest, a median one, a random one): h, a and y of all
-    their rows, and in the backward pass dx_perm rows and dW1, db1, dW2, db2;
+  * sampled experts (the busiest and, at the 1024- and 4096-expert workloads, 16
+    more spread over the row counts; 4 more at the wide workload, whose experts take
+    1 GB each in fp64): h, a and y of all their rows, and in the backward pass
+    dy_perm and dx_perm rows and dW1, db1, dW2, db2;
   * sampled tokens: y, dw, dg and dx, computed by the oracle through the token's
-    own experts;
-  * dWg and dbg need every token's experts, so at these sizes they are checked by
-    a property that holds at any size: the softmax gradient of a token sums to
-    zero, so within each grid dimension the columns of dbg (and of dWg) sum to 0.
+    own experts end to end;
+  * every token, stage by stage from the GPU's own inputs to the stage, in fp64 on
+    the host (Eq. 1 and its derivative): the combine (y from y_perm, w, pos), the
+    combine backward (dy_perm and dw from dy, y_perm, w, pos), the softmax gradient
+    (dg from w, dw), the dispatch backward (dx from dx_perm, pos and the gate's share
+    dg Wg) and the gate layers' gradients (dWg = ds^T x and dbg = sum_t ds, ds built
+    from dg and idx).  The bounds are those of the arithmetic: fp32 sums in a fixed
+    order and one rounding to the stored dtype.
 """
 import gc
 
@@ -32,6 +38,89 @@ BIG = ["tfm_fwd", "tfm_fail_skew", "grid3d", "wide"]
 def _free():
     gc.collect()
     torch.cuda.empty_cache()
+
+
+U32, U_BF16 = 2.0 ** -24, 2.0 ** -8      # fp32 unit roundoff; bf16 half-ulp relative bound
+
+
+def _within(gpu, ref, bound, name):
+    g = O.to64(gpu)
+    assert g.shape == ref.shape, (name, g.shape, ref.shape)
+    assert np.isfinite(g).all(), f"{name}: non-finite values"
+    bad = np.abs(g - ref) > bound
+    if bad.any():
+        i = np.unravel_index(np.argmax(np.abs(g - ref) - bound), g.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())}/{bad.size} beyond the bound; worst at {i}: "
+                             f"gpu {g[i]!r} ref {ref[i]!r} bound {bound[i]!r}")
+
+
+def stage_checks(wl, L, x, dy, Wg, alive_h, dWg=None, dbg=None, chunk=1024):
+    """Every token, each stage from the GPU's own inputs to it (fp64 on the host).
+    fp32 accumulation of n terms in a fixed order is within n u sum|terms| of the
+    exact sum (u = 2^-24, each product rounded once more), and a bf16 output adds
+    one rounding of at most 2^-8 of its value."""
+    T, k, D, d, M = wl.T, wl.k, wl.D, wl.d, wl.M
+    bf = wl.dtype == "bf16"
+    r_out = U_BF16 if bf else U32
+    idx_h = L.idx.cpu().numpy()
+    pos_h = L.pos.cpu().numpy()
+    w_h = L.w.cpu().numpy().astype(np.float64)
+    valid = pos_h >= 0
+    # grid digits of every chosen expert (u_0 most significant)
+    digits = np.stack([(idx_h // M ** (d - 1 - i)) % M for i in range(d)], axis=-1)     # [T, k, d]
+    if wl.backward:
+        dw_h = L.dw.cpu().numpy().astype(np.float64)
+        dg_h = L.dg.cpu().numpy().astype(np.float64)
+        # softmax gradient over the alive chosen experts: dg = w (dw - sum_l w_l dw_l)
+        wd = np.where(valid, w_h * dw_h, 0.0)
+        s = wd.sum(axis=1, keepdims=True)
+        dg_ref = np.where(valid, w_h * (dw_h - s), 0.0)
+        mag = np.where(valid, np.abs(w_h) * (np.abs(dw_h) + np.abs(wd).sum(axis=1, keepdims=True)), 0.0)
+        _within(L.dg, dg_ref, (k + 3) * 2 * U32 * mag + 1e-30, "dg (every token)")
+        Wg64 = O.to64(Wg)
+    for t0 in range(0, T, chunk):
+        t1 = min(T, t0 + chunk)
+        p = L.pos[t0:t1].long()
+        pc = p.clamp(min=0)
+        v = valid[t0:t1]
+        wv = np.where(v, w_h[t0:t1], 0.0)
+        yp = O.to64(L.y_perm[pc.reshape(-1)]).reshape(t1 - t0, k, D)                    # rows of the pairs
+        terms = wv[:, :, None] * yp
+        y_ref = terms.sum(axis=1)
+        bound = r_out * np.abs(y_ref) + (k + 2) * 2 * U32 * np.abs(terms).sum(axis=1) + 1e-30
+        _within(L.y[t0:t1], y_ref, bound, f"y (combine, tokens {t0}..{t1})")
+        if not wl.backward:
+            continue
+        dy64 = O.to64(dy[t0:t1])
+        # combine backward: dy_perm rows = w dy (one fp32 product, one rounding), dw = <dy, y_perm row>
+        dyp_ref = wv[:, :, None] * dy64[:, None, :]
+        dyp = O.to64(L.dy_perm[pc.reshape(-1)]).reshape(t1 - t0, k, D)
+        dyp = np.where(v[:, :, None], dyp, 0.0)
+        _within(dyp, dyp_ref, (r_out + 2 * U32) * np.abs(dyp_ref) + 1e-30, f"dy_perm (tokens {t0}..{t1})")
+        prod = dy64[:, None, :] * yp
+        dw_ref = np.where(v, prod.sum(axis=2), 0.0)
+        gD = D * U32 / (1 - D * U32)
+        _within(L.dw[t0:t1], dw_ref, 2 * gD * np.abs(prod).sum(axis=2) + 1e-30, f"dw (tokens {t0}..{t1})")
+        # dispatch backward: dx = sum over alive pairs of dx_perm rows + sum_j dg_j sum_i Wg[i M + u_i]
+        dxp = O.to64(L.dx_perm[pc.reshape(-1)]).reshape(t1 - t0, k, D)
+        dxp = np.where(v[:, :, None], dxp, 0.0)
+        gate_rows = Wg64[(np.arange(d) * M)[None, None, :] + digits[t0:t1]]                # [t, k, d, D]
+        gterm = dg_h[t0:t1, :, None, None] * gate_rows
+        dx_ref = dxp.sum(axis=1) + gterm.sum(axis=(1, 2))
+        mag = np.abs(dxp).sum(axis=1) + np.abs(gterm).sum(axis=(1, 2))
+        _within(L.dx[t0:t1], dx_ref, r_out * np.abs(dx_ref) + (k + k * d + 2) * 2 * U32 * mag + 1e-30,
+                f"dx (dispatch backward, tokens {t0}..{t1})")
+    if wl.backward and dWg is not None:
+        # gate layers: ds[t, i M + u_i(idx[t, j])] += dg[t, j]; dWg = ds^T x, dbg = sum_t ds
+        ds = np.zeros((T, d * M))
+        for j in range(k):
+            for i in range(d):
+                np.add.at(ds, (np.arange(T), i * M + digits[:, j, i]), dg_h[:, j])
+        x64 = O.to64(x)
+        rtol = RTOL[wl.dtype]
+        assert_close(dWg, ds.T @ x64, rtol, "dWg (every token)")
+        if dbg is not None:
+            assert_close(dbg, ds.sum(axis=0), rtol, "dbg (every token)")
 
 
 @pytest.mark.parametrize("name", BIG)
@@ -103,7 +192,9 @@ def test_fullsize_parity(name):
     # ---------------------------------------------------------------- sampled experts
     rng = np.random.default_rng(0)
     by_count = live[np.argsort(-counts[live], kind="stable")]
-    sample_e = sorted({int(by_count[0]), int(by_count[len(by_count) // 2]), int(rng.choice(live))})
+    more = 4 if wl.D * wl.H > (1 << 24) else 16        # the wide experts take 1 GB each in fp64
+    spread = by_count[np.linspace(1, len(by_count) - 1, more).astype(int)]
+    sample_e = sorted({int(by_count[0])} | {int(e) for e in spread})
     for e in sample_e:
         lo, hi = int(offsets[e]), int(offsets[e + 1])
         E1, c1, E2, c2 = expert(e)
@@ -124,6 +215,7 @@ def test_fullsize_parity(name):
             assert_close(dW2[e], gW2, rtol, f"dW2[{e}]")
             assert_close(db2[e], gb2, rtol, f"db2[{e}]")
         say(f"[fullsize] {name}: expert {e} ({hi - lo} rows) ok")
+        cache.pop(e, None)
     if wl.backward:
         dead = np.nonzero(counts == 0)[0]
         for e in dead[:3]:
@@ -168,15 +260,10 @@ def test_fullsize_parity(name):
         assert_close(L.dw[tsel], np.array(dw_ref), rtol, "dw (sampled tokens)")
         assert_close(L.dg[tsel], np.array(dg_ref), rtol, "dg (sampled tokens)")
         assert_close(L.dx[tsel], np.array(dx_ref), rtol, "dx (sampled tokens)")
-        # softmax gradients sum to zero per token -> per grid dimension, dbg and dWg columns sum to 0
-        dbg_h, dWg_h = O.to64(dbg), O.to64(dWg)
-        for i in range(wl.d):
-            blk = slice(i * wl.M, (i + 1) * wl.M)
-            assert abs(dbg_h[blk].sum()) <= rtol * np.abs(dbg_h[blk]).sum() + 1e-30, f"dbg dim {i}"
-            col = dWg_h[blk].sum(axis=0)
-            assert np.abs(col).max() <= rtol * np.abs(dWg_h[blk]).sum(axis=0).max() + 1e-30, f"dWg dim {i}"
-        assert np.abs(dWg_h).max() > 0
     say(f"[fullsize] {name}: sampled tokens {toks} ok")
+    cache.clear()
+    stage_checks(wl, L, x, dy, Wg, alive_h, dWg if wl.backward else None, dbg if wl.backward else None)
+    say(f"[fullsize] {name}: every-token stage checks ok")
     del L, W1, b1, W2, b2, x, dy
     if wl.backward:
         del dW1, db1, dW2, db2, dWg, dbg
@@ -192,7 +279,9 @@ def test_fullsize_ffblock():
     kernels and launch shapes do not depend on these values.  Checked: routing and
     dispatch of every token; every kept tensor, row gradient and parameter gradient
     of two sampled experts (the busiest and a median one); y, dw, dg and dx of sampled
-    tokens through single-row evaluations of their experts."""
+    tokens through single-row evaluations of their experts; and every token's combine,
+    combine backward, softmax gradient, dispatch backward and gate-layer gradients
+    from the GPU's own inputs to each stage (stage_checks)."""
     import dataclasses
     from paper_2002_04013_amd import DMoEBlockLayer
     from workloads import BLOCK_PARAMS, make_block_experts
@@ -296,5 +385,8 @@ def test_fullsize_ffblock():
     assert_close(L.dg[tsel], np.array(dg_ref), rtol, "dg (sampled tokens)")
     assert_close(L.dx[tsel], np.array(dx_ref), rtol, "dx (sampled tokens)")
     say(f"[fullsize] ffblock: sampled tokens {toks} ok")
+    cache.clear()
+    stage_checks(wl, L, x, dy, Wg, alive_h, dWg, dbg)
+    say("[fullsize] ffblock: every-token stage checks ok")
     del L, prm, grads, x, dy
     _free()
