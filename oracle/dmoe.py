@@ -107,38 +107,37 @@ def topk_bruteforce(S32, d, M, k):
     return order.astype(np.int64), np.take_along_axis(g, order, axis=1)
 
 
-def _topk_list(items, scores, k):
-    """The TopK helper of App. C: sort by score (ties: lexicographically smaller uid
-    prefix first, i.e. lower flat index) and keep at most k."""
-    order = sorted(range(len(items)), key=lambda n: (-scores[n], items[n]))
-    order = order[:k]
-    return [items[n] for n in order], [scores[n] for n in order]
-
-
-def topk_beam(S32, d, M, k, active_suffixes=None):
-    """Algorithm 1 (SelectExperts, App. C): start from the k best indices of grid
-    dimension 0, then add one dimension at a time, extending each kept prefix by
-    its active suffixes, adding g_i(x, j) to the prefix score, and keeping the k
-    best prefixes.  active_suffixes(prefix_tuple) -> iterable of next indices;
-    None means every index of the dimension is active (fully populated grid)."""
+def topk_beam(S32, d, M, k, active=None):
+    """The dimension-by-dimension search of Algorithm 1 (App. C), for all tokens at
+    once.  A beam of at most k uid prefixes (as flat codes of their leading digits)
+    starts as the k best indices of grid dimension 0 by their score g_0; dimension i
+    then extends every kept prefix by each index j whose longer prefix leads to an
+    expert that exists, the candidate's score being the prefix score plus g_i(x)[j]
+    (fp64, in dimension order), and keeps the k best candidates, ties to the
+    lexicographically smaller prefix.  active: bool [M**d] marking the experts that
+    exist, or None for the fully populated grid.  Raises if some token's beam ends
+    with fewer than k prefixes."""
     S32 = np.asarray(S32)
     T = S32.shape[0]
-    out_idx, out_g = [], []
-    for t in range(T):
-        beam = [(u,) for u in range(M)]
-        scores = [float(np.float64(S32[t, u])) for u in range(M)]
-        beam, scores = _topk_list(beam, scores, k)
-        for i in range(1, d):
-            nb, ns = [], []
-            for prefix, sc in zip(beam, scores):
-                suffixes = range(M) if active_suffixes is None else active_suffixes(prefix)
-                for j in suffixes:
-                    nb.append(prefix + (j,))
-                    ns.append(sc + float(np.float64(S32[t, i * M + j])))
-            beam, scores = _topk_list(nb, ns, k)
-        out_idx.append([int(flat_index(b, M)) for b in beam])
-        out_g.append(scores)
-    return np.array(out_idx, np.int64), np.array(out_g, np.float64)
+    exists = np.ones(M ** d, bool) if active is None else np.asarray(active, bool).reshape(-1)
+    codes = np.broadcast_to(np.arange(M), (T, M))
+    score = S32[:, :M].astype(np.float64)
+    keep = np.lexsort((codes, -score), axis=-1)[:, :k]
+    codes, score = np.take_along_axis(codes, keep, 1), np.take_along_axis(score, keep, 1)
+    live = np.ones(codes.shape, bool)
+    for i in range(1, d):
+        # a prefix of i+1 digits leads to an expert if any cell below it exists
+        reach = exists.reshape(M ** (i + 1), -1).any(axis=1)
+        cand = (codes[:, :, None] * M + np.arange(M)).reshape(T, -1)
+        csc = (score[:, :, None] + S32[:, None, i * M:(i + 1) * M].astype(np.float64)).reshape(T, -1)
+        ok = (live[:, :, None] & reach[(codes[:, :, None] * M + np.arange(M))]).reshape(T, -1)
+        # usable candidates first, then score descending, then the smaller prefix
+        keep = np.lexsort((cand, -np.where(ok, csc, 0.0), ~ok), axis=-1)[:, :k]
+        codes, score = np.take_along_axis(cand, keep, 1), np.take_along_axis(csc, keep, 1)
+        live = np.take_along_axis(ok, keep, 1)
+    if not live.all() or codes.shape[1] < k:
+        raise ValueError("fewer than k experts reachable by the beam")
+    return codes.astype(np.int64), score
 
 
 def topk_alive_bruteforce(S32, d, M, k, alive):

@@ -50,8 +50,10 @@ def test_golden_appC_six_experts():
     for item in kv["active"]:
         p, suf = item.split(":")
         table[(int(p),)] = [int(s) for s in suf.split(",")]
-    active = lambda prefix: table.get(prefix, [])
-    idx, g = O.topk_beam(S32, d, M, k, active_suffixes=active)
+    active = np.zeros(M ** d, bool)
+    for (p,), sufs in table.items():
+        active[[p * M + s for s in sufs]] = True
+    idx, g = O.topk_beam(S32, d, M, k, active=active)
     assert idx[0].tolist() == [int(v) for v in kv["beam_idx"]]
     assert g[0].tolist() == [float(v) for v in kv["beam_g"]]
     # exact best among the six active experts, by brute force over the table
