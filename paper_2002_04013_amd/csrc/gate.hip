@@ -36,11 +36,19 @@ struct GateArgs {
 // amax 2^-23) with delta = gam * ab[c] the bound on the score's accumulation error;
 // the span must stay below 2^25.  Returns false (nothing written) otherwise.
 // CAP: list capacity, at least K1 (the callers pick 5 when K1 <= 5, else KMAX + 1).
-template <bool CERT, int CAP>
+// ALIVE (TopK among the alive experts, with CERT): the K1 = min(N, CAP) best cells are
+// ranked the same way; walking them in order, the first k alive ones are the k best
+// alive experts of the whole grid as soon as the k-th of them lies within those K1 (a
+// cell outside the K1 best is beaten by all of them).  The selection is kept if the
+// k-th alive cell is found there, the totals up to the cell after it are separated by
+// more than 2E (or every cell was ranked), and the span condition holds; otherwise
+// nothing is written (the token goes to the exact alive-first path).
+template <bool CERT, int CAP, bool ALIVE = false>
 __device__ __forceinline__ bool select_token_cap(const double* s64, const float* ab, const uint8_t* alive, int d,
                                                  int M, int k, int N, float gam, int32_t* idx_out, float* w_out,
                                                  float* g_out) {
-  const int K1 = CERT && k < N ? k + 1 : k;
+  static_assert(!ALIVE || CERT, "alive-first selection on certified MFMA scores");
+  const int K1 = ALIVE ? (N < CAP ? N : CAP) : (CERT && k < N ? k + 1 : k);
   const int L = K1 < M ? K1 : M;
   float lv[DMAX][CAP];
   int li[DMAX][CAP];
@@ -148,7 +156,40 @@ __device__ __forceinline__ bool select_token_cap(const double* s64, const float*
       }
     }
   }
-  if constexpr (CERT) {
+  if constexpr (ALIVE) {
+    // the first k alive cells among the K1 best; position of the k-th
+    int pk = -1, cnt = 0;
+#pragma unroll
+    for (int p = 0; p < CAP; ++p) {
+      const bool live = p < K1 && cnt < k && (alive == nullptr || alive[tf[p]] != 0);
+      if (live) {
+        ++cnt;
+        if (cnt == k) pk = p;
+      }
+    }
+    if (pk < 0) return false;
+    if (pk + 1 >= K1 && K1 < N) return false;      // the cell after the k-th is not ranked
+    const double E = (double)d * ((double)dmax + (double)amax * 1.1920928955078125e-7);
+    bool sep = true;
+#pragma unroll
+    for (int j = 0; j + 1 < CAP; ++j)
+      if (j <= pk && j + 1 < K1) sep = sep && (tv[j] - tv[j + 1] > 2.0 * E);
+    if (!sep) return false;
+    // keep only the alive cells, in order: compact positions 0 .. pk
+    int w = 0;
+#pragma unroll
+    for (int p = 0; p < CAP; ++p) {
+      if (p <= pk && (alive == nullptr || alive[tf[p]] != 0)) {
+        // move entry p to slot w (w <= p): selects over the register arrays
+        const double vv = tv[p];
+        const int ff = tf[p], uu = tu[p];
+#pragma unroll
+        for (int q = 0; q < CAP; ++q)
+          if (q == w) { tv[q] = vv; tf[q] = ff; tu[q] = uu; }
+        ++w;
+      }
+    }
+  } else if constexpr (CERT) {
     const double E = (double)d * ((double)dmax + (double)amax * 1.1920928955078125e-7);
     bool sep = true;
 #pragma unroll
@@ -193,9 +234,13 @@ __device__ __forceinline__ bool select_token_cap(const double* s64, const float*
   return true;
 }
 
-template <bool CERT>
+template <bool CERT, bool ALIVE = false>
 __device__ __forceinline__ bool select_token(const double* s64, const float* ab, const uint8_t* alive, int d, int M,
                                              int k, int N, float gam, int32_t* idx_out, float* w_out, float* g_out) {
+  if constexpr (ALIVE) {      // k + 3 cells ranked: up to two dead ones ahead of the k-th alive
+    if (k <= 4) return select_token_cap<true, 7, true>(s64, ab, alive, d, M, k, N, gam, idx_out, w_out, g_out);
+    return select_token_cap<true, KMAX + 3, true>(s64, ab, alive, d, M, k, N, gam, idx_out, w_out, g_out);
+  }
   const int K1 = CERT && k < N ? k + 1 : k;
   if (K1 <= 5) return select_token_cap<CERT, 5>(s64, ab, alive, d, M, k, N, gam, idx_out, w_out, g_out);
   return select_token_cap<CERT, KMAX + 1>(s64, ab, alive, d, M, k, N, gam, idx_out, w_out, g_out);
@@ -319,7 +364,9 @@ __device__ __forceinline__ void g2l16(const void* g, void* lds_wave_base) {
 // operands (the contraction order is permuted identically for x and Wg).  The
 // waves' fp64 partial sums are added in wave order in LDS, then one lane per token
 // selects.
-template <int CB, int KW>              // 32-column blocks of the d*M gate columns; waves
+// ALIVE: TopK among the alive experts (the certified selection extended until k alive
+// cells are decided; see select_token_cap).
+template <int CB, int KW, bool ALIVE = false>   // 32-column blocks of the d*M gate columns; waves
 __global__ void __launch_bounds__(64 * KW) gate_topk_mfma(GateMfmaArgs ga) {
   const GateArgs& a = ga.a;
   extern __shared__ __align__(1024) unsigned char sm[];
@@ -443,7 +490,7 @@ __global__ void __launch_bounds__(64 * KW) gate_topk_mfma(GateMfmaArgs ga) {
   }
   if (threadIdx.x < GM_TOK && t0 + (int)threadIdx.x < a.T) {
     const int t = t0 + threadIdx.x;
-    const bool ok = select_token<true>(s64 + lane * SLD, ab + lane * SLD, a.alive, a.d, a.M, a.k, a.N, ga.gam,
+    const bool ok = select_token<true, ALIVE>(s64 + lane * SLD, ab + lane * SLD, a.alive, a.d, a.M, a.k, a.N, ga.gam,
                                        a.idx + (int64_t)t * a.k, a.w + (int64_t)t * a.k,
                                        a.g ? a.g + (int64_t)t * a.k : nullptr);
     if (!ok) ga.queue[GQ_HEAD + atomicAdd(ga.queue, 1)] = t;
@@ -761,12 +808,14 @@ __global__ void __launch_bounds__(GX_NT) gate_exact_kernel(GateArgs a, const int
 }
 
 // The tokens the certificate rejects (bf16 MFMA scores): one token a pass, two blocks
-// per compute unit.
+// per compute unit.  ALIVE: ranked alive first.
+template <bool ALIVE>
 __global__ void __launch_bounds__(GX_NT) __attribute__((amdgpu_waves_per_eu(4)))
 gate_exact_sparse_kernel(GateArgs a, const int32_t* queue) {
   __shared__ double s64[1][DM_MAX];
   __shared__ double sd[1][DM_MAX];
-  exact_body<bf16, false, 1>(a, queue, s64, sd, nullptr);
+  __shared__ uint8_t alv[ALIVE ? NMAX : 1];
+  exact_body<bf16, ALIVE, 1>(a, queue, s64, sd, ALIVE ? alv : nullptr);
 }
 
 // every token into the queue (the exact path for all of them)
@@ -922,7 +971,9 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
   if (!aligned16(x) || !aligned16(Wg)) return DMOE_EUNSUPPORTED;
   GateArgs a{x, Wg, bg, alive, idx, w, g, scores, (int)s.T, (int)s.D, s.d, s.M, s.k, (int)s.dM, (int)s.N};
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (s.flags & DMOE_FLAG_ALIVE_TOPK) {
+  const bool alive_first = (s.flags & DMOE_FLAG_ALIVE_TOPK) != 0;
+  const bool mfma = s.dtype == DMOE_BF16 && s.dM <= 3 * 32;
+  if (alive_first && (!mfma || (s.flags & DMOE_FLAG_GATE_EXACT))) {
     // TopK among the alive experts: exact scores and a ranking of every cell
     if (!ws) return DMOE_EINVAL;
     if (!aligned16(ws)) return DMOE_EUNSUPPORTED;
@@ -935,7 +986,7 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
       DMOE_LAUNCH((gate_exact_kernel<float, true>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
     return launch_status();
   }
-  if (s.dtype == DMOE_BF16 && s.dM <= 3 * 32) {
+  if (mfma) {
     if (!ws) return DMOE_EINVAL;
     if (!aligned16(ws)) return DMOE_EUNSUPPORTED;
     // error factor of the MFMA scores (see the certificate above gate_topk_mfma)
@@ -947,8 +998,12 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
     const int KW = gm_kw(s.D);
     const size_t lds = gate_mfma_lds_bytes((int)s.dM, KW);
     const int CB = (int)((s.dM + 31) / 32);
-    auto kern = KW == 2 ? (CB == 1 ? gate_topk_mfma<1, 2> : CB == 2 ? gate_topk_mfma<2, 2> : gate_topk_mfma<3, 2>)
-                        : (CB == 1 ? gate_topk_mfma<1, 1> : CB == 2 ? gate_topk_mfma<2, 1> : gate_topk_mfma<3, 1>);
+    auto pick = [&](auto AL) {
+      constexpr bool A = decltype(AL)::value;
+      return KW == 2 ? (CB == 1 ? gate_topk_mfma<1, 2, A> : CB == 2 ? gate_topk_mfma<2, 2, A> : gate_topk_mfma<3, 2, A>)
+                     : (CB == 1 ? gate_topk_mfma<1, 1, A> : CB == 2 ? gate_topk_mfma<2, 1, A> : gate_topk_mfma<3, 1, A>);
+    };
+    auto kern = alive_first ? pick(std::true_type{}) : pick(std::false_type{});
     if (lds > 65536) {
       (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       (void)hipGetLastError();
@@ -962,7 +1017,8 @@ extern "C" int dmoe_gate_topk(const dmoe_dims* dims, const void* x, const void* 
       DMOE_LAUNCH((gate_exact_kernel<bf16, false>), dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
     } else {
       const int xgrid = (int)std::min<int64_t>(s.T, 1024);
-      DMOE_LAUNCH(gate_exact_sparse_kernel, dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+      if (alive_first) DMOE_LAUNCH(gate_exact_sparse_kernel<true>, dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
+      else DMOE_LAUNCH(gate_exact_sparse_kernel<false>, dim3(xgrid), dim3(GX_NT), 0, st, a, queue);
     }
   } else {
     // fp32, and bf16 with more than 96 gate columns: exact fp64 scores for every token
