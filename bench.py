@@ -218,13 +218,13 @@ def cpu_baseline(wl, inp, counts, budget_s=12.0, max_experts=16):
             "seconds_measured": round(t_route + t_exp, 3)}
 
 
-def cpu_baselines(wl, inp, counts):
+def cpu_baselines(wl, inp, counts, budget_s=12.0, one_budget_s=8.0):
     """The oracle on the host's BLAS threads, then on one thread (smaller sample)."""
-    out = cpu_baseline(wl, inp, counts)
+    out = cpu_baseline(wl, inp, counts, budget_s=budget_s)
     try:
         from threadpoolctl import threadpool_limits
         with threadpool_limits(limits=1, user_api="blas"):
-            one = cpu_baseline(wl, inp, counts, budget_s=8.0, max_experts=4)
+            one = cpu_baseline(wl, inp, counts, budget_s=one_budget_s, max_experts=4)
         out["one_thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample", "seconds_measured")}
     except Exception as ex:  # threadpoolctl missing: report the main figure only
         out["one_thread"] = {"error": str(ex)}
@@ -280,10 +280,11 @@ def log(msg):
 
 
 def run_workload(name, steps, warmup, recompute=False, sgd=False, alive_topk=False, cold_steps=0,
-                 cpu=False):
+                 cpu=False, cpu_budget=(12.0, 8.0)):
     """Build one workload's inputs and layer, time `steps` steps after `warmup`, trace
-    every kernel in the timed region, optionally time `cold_steps` more steps each after
-    a cache flush, and return the measurements."""
+    every kernel in the timed region, time a few more steps with call-boundary events
+    only, optionally time `cold_steps` more steps each after a cache flush, and return
+    the measurements."""
     import torch
     from paper_2002_04013_amd import DMoEBlockLayer, DMoELayer, abi
     from workloads import (get_workload, make_alive, make_block_experts, make_dy, make_experts, make_gate,
@@ -403,11 +404,27 @@ def run_workload(name, steps, warmup, recompute=False, sgd=False, alive_topk=Fal
            "call_roofline": {n: call_roof(n) for n in timed}, "alg": alg, "peak_tf": peak_tf,
            "traced": trace.count, "inp_host": None}
 
+    # The calls once more with call-boundary events only: the trace's event after every
+    # kernel adds a few microseconds at each kernel boundary, a visible share of the
+    # short calls (gate, dispatch, combine), so their fractions come from these steps.
+    n_u = min(steps, 5)
+    uev = new_events(n_u)
+    for i in range(n_u):
+        step(uev[i])
+    torch.cuda.synchronize()
+    ms_u = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in uev) / n_u for n in timed}
+    out["ms_untraced"] = ms_u
+    out["per_step_untraced"] = sorted(e[timed[0]][0].elapsed_time(e[timed[-1]][1]) for e in uev)
+    out["call_roofline_untraced"] = {n: roofline_of(alg[n]["flops"], alg[n]["bytes"], ms_u[n] * 1e-3, peak_tf)
+                                     for n in timed}
+
     if cold_steps:
         # Cold memory-side cache: before each step, outside any timed interval, write
         # FLUSH_BYTES to one scratch buffer and read FLUSH_BYTES from another, so the
         # step's first reads (the gate's x) come from HBM and no dirty lines of the
         # previous step are left to write back.
+        # The calls are timed untraced (call-boundary events only); the main kernels'
+        # durations come from as many traced cold steps after them.
         fw = torch.empty(FLUSH_BYTES // 2, dtype=torch.int16, device=dev)
         fr = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
         cev = new_events(cold_steps)
@@ -416,8 +433,12 @@ def run_workload(name, steps, warmup, recompute=False, sgd=False, alive_topk=Fal
         for i in range(cold_steps):
             fw.fill_(i)
             sink += fr.sum()
+            step(cev[i])
+        for i in range(cold_steps):
+            fw.fill_(i + cold_steps)
+            sink += fr.sum()
             with ctrs[i]:
-                step(cev[i])
+                step()
         torch.cuda.synchronize()
         cms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in cev) / cold_steps for n in ("gate_topk", "dispatch")}
         ck = {}
@@ -427,8 +448,9 @@ def run_workload(name, steps, warmup, recompute=False, sgd=False, alive_topk=Fal
                     ck.setdefault(kname, []).append(t)
         cold = {}
         for n in ("gate_topk", "dispatch"):
-            warm_r, cold_r = call_roof(n), roofline_of(alg[n]["flops"], alg[n]["bytes"], cms[n] * 1e-3, peak_tf)
-            cold[n] = {"warm_ms": round(ms[n], 4), "cold_ms": round(cms[n], 4),
+            warm_r = out["call_roofline_untraced"][n]
+            cold_r = roofline_of(alg[n]["flops"], alg[n]["bytes"], cms[n] * 1e-3, peak_tf)
+            cold[n] = {"warm_ms": round(ms_u[n], 4), "cold_ms": round(cms[n], 4),
                        "warm_frac": warm_r["frac"], "cold_frac": cold_r["frac"], "bound": cold_r["bound"],
                        "cold_achieved": cold_r["achieved"], "unit": cold_r["unit"]}
         for kname, ts in ck.items():
@@ -439,14 +461,16 @@ def run_workload(name, steps, warmup, recompute=False, sgd=False, alive_topk=Fal
                                                                  if k in r}}
         out["cold"] = cold
         out["cold_protocol"] = (f"before each of {cold_steps} steps, outside the timed calls: write "
-                                f"{FLUSH_BYTES >> 20} MiB, then read another {FLUSH_BYTES >> 20} MiB")
+                                f"{FLUSH_BYTES >> 20} MiB, then read another {FLUSH_BYTES >> 20} MiB; "
+                                f"calls timed with call-boundary events only, kernels in {cold_steps} more "
+                                f"such steps with the per-kernel trace")
         del fw, fr
 
     if cpu:
         host = {n: v for n, v in inp.items()}
         for n in ("x", "dy", "Wg", "bg", "alive"):
             host[n] = inp[n].cpu()
-        out["cpu_baseline"] = cpu_baselines(wl, host, counts)
+        out["cpu_baseline"] = cpu_baselines(wl, host, counts, *cpu_budget)
     del inp, L, calls, step
     return out
 
@@ -471,16 +495,21 @@ def summary(r, steps):
            "tokens_per_s": round(wl.T * steps / r["wall"], 1),
            "step_device_ms_median": round(r["per_step"][len(r["per_step"]) // 2], 4),
            "calls_ms": {n: round(v, 4) for n, v in r["ms"].items()},
+           "calls_ms_untraced": {n: round(v, 4) for n, v in r["ms_untraced"].items()},
            "calls_roofline": {n: {k: v[k] for k in ("bound", "achieved", "unit", "frac")}
-                              for n, v in r["call_roofline"].items()},
+                              for n, v in r["call_roofline_untraced"].items()},
            "rows_used": rows, "max_rows_per_expert": int(max(r["counts"])),
            "experts_without_rows": int(sum(1 for c in r["counts"] if c == 0)),
            "top_kernels": r["kernels"][:6]}
     if wl.name == "tiny_f32":
         out["step_device_us_median"] = round(r["per_step"][len(r["per_step"]) // 2] * 1e3, 1)
+        pu = r["per_step_untraced"]
+        out["step_device_us_median_untraced"] = round(pu[len(pu) // 2] * 1e3, 1)
     if "cold" in r:
         out["cold"] = r["cold"]
         out["cold_protocol"] = r["cold_protocol"]
+    if "cpu_baseline" in r:
+        out["cpu_baseline"] = r["cpu_baseline"]
     return out
 
 
@@ -554,9 +583,12 @@ def main():
         "kernels": kernels,
         "roofline_ffn_fwd": r["call_roofline"]["ffn_fwd"],
         "roofline_ffn_bwd": r["call_roofline"].get("ffn_bwd"),
-        "gate_topk": r["call_roofline"]["gate_topk"],
-        "dispatch": r["call_roofline"]["dispatch"],
+        "gate_topk": r["call_roofline_untraced"]["gate_topk"],
+        "dispatch": r["call_roofline_untraced"]["dispatch"],
         "calls_ms": {n: round(v, 4) for n, v in ms.items()},
+        "calls_ms_untraced": {n: round(v, 4) for n, v in r["ms_untraced"].items()},
+        "calls_timing": ("calls_ms: the timed steps, with an event after every kernel; calls_ms_untraced, "
+                         "gate_topk and dispatch: 5 more steps with events at call boundaries only"),
         "step_ms": {"median": round(r["per_step"][len(r["per_step"]) // 2], 3), "min": round(r["per_step"][0], 3),
                     "max": round(r["per_step"][-1], 3)},
         "paper_context": PAPER_CONTEXT,
@@ -576,7 +608,8 @@ def main():
             if name == args.workload:
                 continue
             st = 20 if name == "tiny_f32" else 5
-            rr = run_workload(name, st, 2, cold_steps=3 if name in COLD_WORKLOADS else 0)
+            rr = run_workload(name, st, 2, cold_steps=3 if name in COLD_WORKLOADS else 0,
+                              cpu=not args.no_cpu_baseline, cpu_budget=(3.0, 3.0))
             extra[name] = summary(rr, st)
             del rr
             gc.collect()

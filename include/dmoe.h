@@ -28,11 +28,17 @@
  *   - Buffers are sized for P_max rows; the number of rows actually used,
  *     offsets[N], stays on the device (no host synchronisation on the path).
  *   - Results are bitwise reproducible from run to run (no floating-point atomics).
-   - Workspace contents need no initialisation: an entry point reads only workspace
-     memory it has written itself (counters are cleared by kernels, not memsets).
-   - The calls can be recorded into a HIP graph by stream capture and replayed (no
-     allocation, synchronisation or memset node); a replay computes what the eager
-     calls compute, bit for bit.
+ *   - Workspace contents need no initialisation: an entry point reads only workspace
+ *     memory it has written itself (counters are cleared by kernels, not memsets).
+ *   - The calls can be recorded into a HIP graph by stream capture and replayed (no
+ *     allocation, synchronisation or memset node); a replay computes what the eager
+ *     calls compute, bit for bit.
+ *   - Process state: the library keeps three things beyond the call.  (1) Per device,
+ *     its compute-unit count and, per kernel, the blocks per compute unit the occupancy
+ *     query reports; both are looked up on first use and cached in atomics (concurrent
+ *     first calls may both look up; they store the same value), so entry points may be
+ *     called from several host threads.  (2) The launch trace below, per host thread.
+ *     (3) The 131328-byte device array of dmoe_expert_ffn_fwd_noalloc, per device.
  *   - Supported: 1 <= d <= 4, 1 <= M, d*M <= 128, 1 <= k <= min(N, 8),
  *     N <= 16384, T >= 0, D and H multiples of 64 and at most 2^22, pointers 16-byte aligned.
  *
@@ -76,7 +82,8 @@ typedef struct {
  * only): cells are ranked by (alive first, g descending, lower flat index) and the k
  * first chosen, so dead experts are taken only when fewer than k are alive (they get
  * weight 0).  Without it, TopK ranks every expert and dead chosen ones get weight 0.
- * With it, every token's gate scores use exact fp64 accumulation. */
+ * The decision is exact either way: a token whose alive-first choice the fast path
+ * cannot certify is recomputed with exact fp64 scores over every cell. */
 enum { DMOE_FLAG_GATE_EXACT = 1, DMOE_FLAG_ALIVE_TOPK = 2 };
 
 /* Bytes of device workspace every entry point below needs for these dims
@@ -241,10 +248,15 @@ int dmoe_expert_ffn_bwd_sgd(const dmoe_dims* dims, const int32_t* offsets, const
                             void* W1, void* b1, void* W2, void* b2, float lr, void* dh,
                             void* dx_perm, void* ws, void* stream);
 
-/* Input gradient of the layer: the experts' input gradients summed over each
- * token's alive pairs (slot order), plus, when idx, dg and Wg are all non-NULL,
- * the gate's share sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])].  fp32 accumulation,
- * one rounding.  dx [T, D] written.  Uses workspace: no. */
+/* Input gradient of the layer (derivative of Eq. 1 with respect to x).  x reaches
+ * the output along two routes: through each chosen alive expert f(x) (the Trainer
+ * sends x to those experts and their Backward returns input gradients, Sec. 3.3), and
+ * through the gate scores g(x, f) = sum_i g_i(x)[u_i] of the Sec. 3.2 gate.  So
+ *   dx[t] = sum_j dx_perm[pos[t,j]]                       (alive pairs, slot order)
+ *         + sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])]   (when idx, dg, Wg are non-NULL)
+ * with dg from dmoe_gate_topk_bwd.  The gate's share is added here rather than in
+ * dmoe_gate_topk_bwd so that dx is written once, in one pass over its T*D elements.
+ * fp32 accumulation, one rounding.  dx [T, D] written.  Uses workspace: no. */
 int dmoe_dispatch_bwd(const dmoe_dims* dims, const void* dx_perm, const int32_t* pos,
                       const int32_t* idx, const float* dg, const void* Wg, void* dx,
                       void* stream);

@@ -35,7 +35,8 @@ struct GateArgs {
 // is kept only if their totals are separated by more than 2E, E = d (delta_max +
 // amax 2^-23) with delta = gam * ab[c] the bound on the score's accumulation error;
 // the span must stay below 2^25.  Returns false (nothing written) otherwise.
-// CAP: list capacity, at least K1 (the callers pick 5 when K1 <= 5, else KMAX + 1).
+// CAP: list capacity, at least K1 (the callers pick 5 when K1 <= 5, else KMAX + 1;
+// for ALIVE 7 when k <= 4, else KMAX + 3).
 // ALIVE (TopK among the alive experts, with CERT): the K1 = min(N, CAP) best cells are
 // ranked the same way; walking them in order, the first k alive ones are the k best
 // alive experts of the whole grid as soon as the k-th of them lies within those K1 (a
