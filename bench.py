@@ -466,6 +466,28 @@ def run_workload(name, steps, warmup, recompute=False, sgd=False, alive_topk=Fal
                                 f"such steps with the per-kernel trace")
         del fw, fr
 
+    if sgd and not block:
+        # What the fused update replaces: the gradient-returning backward, then a separate
+        # SGD step over the same parameters (torch's in-place add, for comparison only).
+        n_c = min(steps, 5)
+        ce = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_c)]
+        for i in range(n_c):
+            ce[i][0].record(stream)
+            abi.dmoe_expert_ffn_bwd(Dm, L.offsets, L.counts, L.x_perm, L.h, L.a, L.dy_perm, W1, W2, L.dh,
+                                    L.dx_perm, dW1, db1, dW2, db2, L.ws)
+            ce[i][1].record(stream)
+            for prm_t, grad_t in ((W1, dW1), (b1, db1), (W2, dW2), (b2, db2)):
+                prm_t.add_(grad_t, alpha=-1e-4)
+            ce[i][2].record(stream)
+        torch.cuda.synchronize()
+        t_b = sum(c[0].elapsed_time(c[1]) for c in ce) / n_c
+        t_u = sum(c[1].elapsed_time(c[2]) for c in ce) / n_c
+        out["sgd_comparison"] = {
+            "fused_sgd_backward_ms": round(ms["ffn_bwd"], 3),
+            "gradient_backward_ms": round(t_b, 3), "separate_update_ms": round(t_u, 3),
+            "gradient_backward_plus_update_ms": round(t_b + t_u, 3),
+            "note": "separate update: torch in-place add of -lr * gradient to W1, b1, W2, b2 (comparison only)"}
+
     if cpu:
         host = {n: v for n, v in inp.items()}
         for n in ("x", "dy", "Wg", "bg", "alive"):
@@ -598,6 +620,8 @@ def main():
         result["cold_protocol"] = r["cold_protocol"]
     if "cpu_baseline" in r:
         result["cpu_baseline"] = r["cpu_baseline"]
+    if "sgd_comparison" in r:
+        result["sgd_comparison"] = r["sgd_comparison"]
     del r
     gc.collect()
     torch.cuda.empty_cache()

@@ -616,6 +616,35 @@ grouped_gemm2(GemmArgs<bf16> p) {
       }
     }
 
+    // SGD with staged stores on a 2-slot ring: ring slot 1 is idle until the next tile's
+    // stage 1 is issued after the epilogue, so each wave passes its fp32 accumulators
+    // through 8 KiB of it, 32 rows x 64 columns at a time, and the update is computed in
+    // the store layout: lane L handles row L/8 + 8q, columns 8(L%8) .. +7 of the piece,
+    // reading the old parameters as whole 128-byte lines one piece ahead of their use.
+    constexpr bool SGD_SLOT = EPI == EPI_SGD && STO != STORE_DIRECT && STAGES == 2 && GM == GROUP_K;
+    static_assert(!SGD_SLOT || (NW * 8192 <= SBYTES && WTN % 64 == 0), "fp32 staging in one ring slot");
+    char* s32 = smem + SBYTES + wave * 8192;
+    // element (r, c) of the 32 x 64 fp32 piece: 16-byte chunk c/4 of row r, XOR-swizzled
+    auto s32_off = [](int r, int ch) { return r * 256 + ((ch ^ (r & 15)) << 4); };
+    constexpr int HP = TN >= 2 ? TN / 2 : 1;    // 64-column pieces per 32-row block
+    const int np = nl * HP;                      // this wave's pieces (uniform)
+    bf16* W = reinterpret_cast<bf16*>(p.C);
+    auto prow = [&](int pc, int qd) {            // parameter row offset of lane's row qd
+      const int ml = ((pc / HP) * WM + wm) * 32 + (lane >> 3) + 8 * qd;
+      return (int64_t)e * p.c_gstride + (int64_t)(m0 + (ml < mvalid ? ml : 0)) * p.ldc;
+    };
+    auto pcol = [&](int pc) {
+      const int col = wn * WTN + 64 * (pc % HP) + 8 * (lane & 7);
+      return n0 + (col < nvalid ? col : 0);
+    };
+    // the parameter loads are issued for every lane (clamped in range); stores only
+    // where the row and column are valid
+    uint4 wold[2][4];
+    auto load_piece = [&](int pc, uint4 (&dst)[4]) {
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd)
+        dst[qd] = *reinterpret_cast<const uint4*>(W + prow(pc, qd) + pcol(pc));
+    };
     if (more) {
       if (early == 0) {
         nxt = setup(L + Lstep);
@@ -727,10 +756,80 @@ grouped_gemm2(GemmArgs<bf16> p) {
         emit_direct(accx, cb, (int64_t)(off + m0 + ml) * p.ldc, mok, bias_x, aux_x);
       }
     }
+    if constexpr (SGD_SLOT) {
+      // one piece: stage its accumulators, read them back in the store layout, update
+      // and store (GUARD: some rows or columns of the tile are past the matrix); the
+      // waits for the parameter loads are the compiler's, per register
+      auto piece = [&](auto GUARDc, int pc, int buf) {
+        constexpr bool GUARD = decltype(GUARDc)::value;
+        const int j = pc / HP, h = pc % HP;
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x16_t& a = acc[2 * h + ii][j];
+            *reinterpret_cast<float4*>(s32 + s32_off(l32, ii * 8 + 2 * g + lhi)) =
+                make_float4(a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]);
+          }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        float v[4][8];
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const int r = (lane >> 3) + 8 * qd, c8 = lane & 7;
+          const float4 lo = *reinterpret_cast<const float4*>(s32 + s32_off(r, 2 * c8));
+          const float4 hi = *reinterpret_cast<const float4*>(s32 + s32_off(r, 2 * c8 + 1));
+          v[qd][0] = lo.x; v[qd][1] = lo.y; v[qd][2] = lo.z; v[qd][3] = lo.w;
+          v[qd][4] = hi.x; v[qd][5] = hi.y; v[qd][6] = hi.z; v[qd][7] = hi.w;
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        const uint4 (&wv)[4] = wold[buf];
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          const uint32_t w4[4] = {wv[qd].x, wv[qd].y, wv[qd].z, wv[qd].w};
+          uint32_t o[4];
+#pragma unroll
+          for (int q2 = 0; q2 < 4; ++q2) {
+            const float a0 = __uint_as_float(w4[q2] << 16) - p.lr * v[qd][2 * q2];
+            const float a1 = __uint_as_float(w4[q2] & 0xffff0000u) - p.lr * v[qd][2 * q2 + 1];
+            o[q2] = f2bf2(a0, a1);
+          }
+          const int ml = (j * WM + wm) * 32 + (lane >> 3) + 8 * qd;
+          const int col = wn * WTN + 64 * h + 8 * (lane & 7);
+          if (!GUARD || (ml < mvalid && col < nvalid)) {
+            uint4* dst = reinterpret_cast<uint4*>(W + (int64_t)e * p.c_gstride + (int64_t)(m0 + ml) * p.ldc + n0 + col);
+            const uint4 ov = make_uint4(o[0], o[1], o[2], o[3]);
+            if constexpr (STO == STORE_STAGED_NT) {
+              typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+              __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, ov), reinterpret_cast<u32x4_t*>(dst));
+            } else {
+              *dst = ov;
+            }
+          }
+        }
+      };
+      if (np == TM * HP && mvalid >= BM && nvalid >= BN) {
+#pragma unroll
+        for (int pc = 0; pc < TM * HP; ++pc) {
+          if (pc == 0) load_piece(0, wold[0]);
+          if (pc + 1 < TM * HP) load_piece(pc + 1, wold[(pc + 1) & 1]);
+          piece(std::false_type{}, pc, pc & 1);
+        }
+      } else {
+#pragma unroll
+        for (int pc = 0; pc < TM * HP; ++pc) {
+          if (pc < np) {
+            load_piece(pc, wold[0]);
+            piece(std::true_type{}, pc, 0);
+          }
+        }
+      }
+      // every wave is done with ring slot 1 before the next tile's stage 1 lands there
+      block_sync_lds();
+    }
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       const int ml = (j * WM + wm) * 32 + l32;
-      if (j >= nl) continue;
+      if (SGD_SLOT || j >= nl) continue;
       int64_t crow;
       if constexpr (GM == GROUP_M) crow = (int64_t)(off + m0 + ml) * p.ldc;
       else crow = (int64_t)e * p.c_gstride + (int64_t)(m0 + ml) * p.ldc;
