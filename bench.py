@@ -275,6 +275,38 @@ def copy_calibration(nbytes=4 << 30, reps=5):
     print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "reps": reps}), flush=True)
 
 
+def vendor_gemm(reps=5):
+    """The vendor library (torch.bmm, hipBLASLt) on the wide workload's expert GEMM shapes,
+    256 experts of exactly 512 rows, bf16, contiguous operands, no epilogue: a reference
+    point for the grouped kernels, not part of the layer."""
+    import torch
+    E = 256
+    shapes = [("up", 512, 4096, 16384), ("down", 512, 16384, 4096),
+              ("dW1 = dh^T x", 16384, 512, 4096), ("dW2 = dy^T a", 4096, 512, 16384)]
+    out = []
+    for name, M, K, N in shapes:
+        A = torch.randn(E, M, K, device="cuda", dtype=torch.bfloat16)
+        B = torch.randn(E, K, N, device="cuda", dtype=torch.bfloat16) * 0.01
+        C = torch.empty(E, M, N, device="cuda", dtype=torch.bfloat16)
+        for _ in range(2):
+            torch.bmm(A, B, out=C)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(reps):
+            torch.bmm(A, B, out=C)
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / reps
+        tf = 2.0 * E * M * K * N / (ms * 1e-3) / 1e12
+        out.append({"gemm": name, "batch": E, "M": M, "K": K, "N": N, "ms": round(ms, 3),
+                    "tflops": round(tf, 1), "frac": round(tf / PEAK_BF16_TFLOPS, 4)})
+        log(f"vendor {name}: {ms:.3f} ms, {tf:.1f} TFLOP/s")
+        del A, B, C
+        torch.cuda.empty_cache()
+    print(json.dumps({"vendor_gemm": out, "library": "torch.bmm (hipBLASLt)"}), flush=True)
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -552,9 +584,14 @@ def main():
                     help="backward updates the expert parameters in place (dmoe_expert_ffn_bwd_sgd, lr 1e-4)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device copy (counter calibration)")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="only time the vendor library's batched GEMM on the wide expert shapes (reference)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.vendor_gemm:
+        vendor_gemm()
         return
     ws_env = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or ws_env != 1:
