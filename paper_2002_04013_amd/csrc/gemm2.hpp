@@ -366,10 +366,21 @@ grouped_gemm2(GemmArgs<bf16> p) {
         // expert after expert (tiles are dealt out in a fixed stride) alternate between
         // the larger and the smaller tiles instead of one group falling steadily behind
         // the other, which would stop them sharing each weight slab in L2.
-        const int nb = (cnt + 31) / 32, qm = (t.e & 1) ? mt_e - 1 - q % mt_e : q % mt_e;
-        const int b0 = qm * nb / mt_e, b1 = (qm + 1) * nb / mt_e;
-        t.m0 = b0 * 32;
-        t.mvalid = cnt - t.m0 < (b1 - b0) * 32 ? cnt - t.m0 : (b1 - b0) * 32;
+        const int qm = (t.e & 1) ? mt_e - 1 - q % mt_e : q % mt_e;
+        if constexpr (B_T) {
+          // N-contiguous weights: the expert's rows split evenly, so its m-tiles issue the
+          // same number of row blocks and stay in step through the whole k loop, sharing
+          // each stage of the weight slab in L2 (a few more rows of padding, measured
+          // faster than splitting whole blocks, which is faster for K-contiguous weights)
+          const int r0 = qm * cnt / mt_e, r1 = (qm + 1) * cnt / mt_e;
+          t.m0 = r0;
+          t.mvalid = r1 - r0;
+        } else {
+          const int nb = (cnt + 31) / 32;
+          const int b0 = qm * nb / mt_e, b1 = (qm + 1) * nb / mt_e;
+          t.m0 = b0 * 32;
+          t.mvalid = cnt - t.m0 < (b1 - b0) * 32 ? cnt - t.m0 : (b1 - b0) * 32;
+        }
       } else {
         t.m0 = (q % mt_e) * BM;
         t.mvalid = cnt - t.m0;
