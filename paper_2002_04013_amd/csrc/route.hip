@@ -16,6 +16,8 @@ namespace dmoe {
 
 constexpr int RT_NT = 256;
 
+template <typename T> struct type_tag { using type = T; };
+
 __global__ void __launch_bounds__(RT_NT)
 dispatch_hist(const int32_t* idx, const uint8_t* alive, int P, int N, int32_t* block_hist) {
   extern __shared__ int hist[];
@@ -231,8 +233,16 @@ __device__ __forceinline__ void store_stream16(void* p, const uint4& v) {
   __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
 }
 
-// dx[t] = sum_j dx_perm[pos[t,j]]  (+ sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])])
-template <typename E>
+// dx[t] = sum_j dx_perm[pos[t,j]]  (+ sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])]), one
+// wave per token.  The gate share is taken over the token's distinct gate columns c,
+// sum_c ds[c] Wg[c] with ds[c] the sum (in term order j, then i from d-1 down) of the dg
+// of the chosen experts whose uid digit selects c: the top cells of a grid share digits,
+// so there are usually about half as many Wg rows to read as terms.  Lane q < d k holds
+// term q; the first lane of each column sums that column's weights; up to GCR columns are
+// then kept in registers for the whole row (KM >= k rows and GC columns; any further
+// columns are read in a loop).  Each 16-byte chunk issues all its loads before adding:
+// rows in slot order, then columns in order of first occurrence.
+template <typename E, int KM, int GCR>
 __global__ void __launch_bounds__(RT_NT)
 dispatch_bwd_kernel(const E* dxp, const int32_t* pos, const int32_t* idx, const float* dg,
                     const E* Wg, E* dx, int T, int D, int k, int d, int M) {
@@ -240,34 +250,88 @@ dispatch_bwd_kernel(const E* dxp, const int32_t* pos, const int32_t* idx, const 
   const int t = blockIdx.x * (RT_NT / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (t >= T) return;
-  int pj[KMAX];
-  for (int j = 0; j < k; ++j) pj[j] = pos[(int64_t)t * k + j];
-  const bool gate = dg != nullptr;
+  int pj[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) pj[j] = j < k ? pos[(int64_t)t * k + j] : -1;
+  // gate columns: term q = j d + (d - 1 - i) on lane q
+  const int nterm = dg != nullptr ? k * d : 0;
+  int mycol = -1;
+  float myw = 0.f;
+  if (lane < nterm) {
+    const int j = lane / d, i = d - 1 - lane % d;
+    int u = idx[(int64_t)t * k + j];
+    for (int r = 0; r < d - 1 - i; ++r) u /= M;
+    mycol = i * M + u % M;
+    myw = dg[(int64_t)t * k + j];
+  }
+  float wsum = 0.f;
+  bool first = lane < nterm;
+  for (int q = 0; q < nterm; ++q) {
+    const int cq = __shfl(mycol, q, 64);
+    const float wq = __shfl(myw, q, 64);
+    if (lane < nterm && cq == mycol) {
+      if (q < lane) first = false;
+      wsum += wq;
+    }
+  }
+  uint64_t fm = __ballot(first);
+  const int ncol = __popcll(fm);
+  // every distinct column also in this wave's LDS list (read by the loop over the
+  // columns past the register cache, which runs in lanes that may have left the chunk
+  // loop's active set, so it cannot take them from other lanes)
+  __shared__ int s_col[RT_NT / 64][KMAX * DMAX];
+  __shared__ float s_w[RT_NT / 64][KMAX * DMAX];
+  const int wv = threadIdx.x >> 6;
+  if (first) {
+    const int slot = __popcll(fm & ((1ull << lane) - 1ull));
+    s_col[wv][slot] = mycol;
+    s_w[wv][slot] = wsum;
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  int gcol[GCR];
+  float gw[GCR];
+#pragma unroll
+  for (int g = 0; g < GCR; ++g) {
+    const int src = fm ? __builtin_ctzll(fm) : 0;
+    gcol[g] = g < ncol ? __shfl(mycol, src, 64) : 0;
+    gw[g] = g < ncol ? __shfl(wsum, src, 64) : 0.f;
+    fm &= fm ? fm - 1 : 0ull;
+  }
   const int CPR = D / VEC;
   for (int c = lane; c < CPR; c += 64) {
+    uint4 rv[KM], gv[GCR];
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+      if (pj[j] >= 0) rv[j] = *reinterpret_cast<const uint4*>(dxp + (int64_t)pj[j] * D + c * VEC);
+#pragma unroll
+    for (int g = 0; g < GCR; ++g)
+      if (g < ncol) gv[g] = *reinterpret_cast<const uint4*>(Wg + (int64_t)gcol[g] * D + c * VEC);
     float acc[VEC];
 #pragma unroll
     for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
-    for (int j = 0; j < k; ++j) {
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
       if (pj[j] < 0) continue;
       float v[VEC];
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(dxp + (int64_t)pj[j] * D + c * VEC), v);
+      Vec<E>::unpack(rv[j], v);
 #pragma unroll
       for (int i = 0; i < VEC; ++i) acc[i] += v[i];
     }
-    if (gate) {
-      for (int j = 0; j < k; ++j) {
-        const float gj = dg[(int64_t)t * k + j];
-        int rem = idx[(int64_t)t * k + j];
-        for (int i = d - 1; i >= 0; --i) {
-          const int col = i * M + rem % M;
-          rem /= M;
-          float v[VEC];
-          Vec<E>::unpack(*reinterpret_cast<const uint4*>(Wg + (int64_t)col * D + c * VEC), v);
 #pragma unroll
-          for (int q = 0; q < VEC; ++q) acc[q] = fmaf(gj, v[q], acc[q]);
-        }
-      }
+    for (int g = 0; g < GCR; ++g) {
+      if (g >= ncol) continue;
+      float v[VEC];
+      Vec<E>::unpack(gv[g], v);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) acc[q] = fmaf(gw[g], v[q], acc[q]);
+    }
+    for (int g = GCR; g < ncol; ++g) {               // rare: more than GCR distinct columns
+      const int col = s_col[wv][g];
+      const float w = s_w[wv][g];
+      float v[VEC];
+      Vec<E>::unpack(*reinterpret_cast<const uint4*>(Wg + (int64_t)col * D + c * VEC), v);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) acc[q] = fmaf(w, v[q], acc[q]);
     }
     store_stream16(dx + (int64_t)t * D + c * VEC, Vec<E>::pack(acc));
   }
@@ -364,15 +428,21 @@ extern "C" int dmoe_dispatch_bwd(const dmoe_dims* dims, const void* dx_perm, con
   if (!aligned16(dx_perm) || !aligned16(dx) || (gate && !aligned16(Wg))) return DMOE_EUNSUPPORTED;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((unsigned)((s.T + 3) / 4));
-  if (s.dtype == DMOE_BF16)
-    DMOE_LAUNCH(dispatch_bwd_kernel<bf16>, grid, dim3(RT_NT), 0, st,
-                       reinterpret_cast<const bf16*>(dx_perm), pos, gate ? idx : nullptr, gate ? dg : nullptr,
-                       reinterpret_cast<const bf16*>(Wg), reinterpret_cast<bf16*>(dx), (int)s.T, (int)s.D, s.k,
-                       s.d, s.M);
-  else
-    DMOE_LAUNCH(dispatch_bwd_kernel<float>, grid, dim3(RT_NT), 0, st,
-                       reinterpret_cast<const float*>(dx_perm), pos, gate ? idx : nullptr, gate ? dg : nullptr,
-                       reinterpret_cast<const float*>(Wg), reinterpret_cast<float*>(dx), (int)s.T, (int)s.D, s.k,
-                       s.d, s.M);
+  auto go = [&](auto EK, auto KMc) {
+    using E = typename decltype(EK)::type;
+    constexpr int KM = decltype(KMc)::value;
+    DMOE_LAUNCH((dispatch_bwd_kernel<E, KM, 8>), grid, dim3(RT_NT), 0, st,
+                reinterpret_cast<const E*>(dx_perm), pos, gate ? idx : nullptr, gate ? dg : nullptr,
+                reinterpret_cast<const E*>(Wg), reinterpret_cast<E*>(dx), (int)s.T, (int)s.D, s.k, s.d, s.M);
+  };
+  using K4 = std::integral_constant<int, 4>;
+  using K8 = std::integral_constant<int, KMAX>;
+  if (s.dtype == DMOE_BF16) {
+    if (s.k <= 4) go(type_tag<bf16>{}, K4{});
+    else go(type_tag<bf16>{}, K8{});
+  } else {
+    if (s.k <= 4) go(type_tag<float>{}, K4{});
+    else go(type_tag<float>{}, K8{});
+  }
   return launch_status();
 }
