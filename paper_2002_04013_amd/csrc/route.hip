@@ -154,29 +154,36 @@ gather_rows(const E* x, const int32_t* pos, int T, int k, int D, E* xp) {
   }
 }
 
-// y[t] = sum_j w[t,j] y_perm[pos[t,j]]; one wave per token.
-template <typename E>
+// y[t] = sum_j w[t,j] y_perm[pos[t,j]]; one wave per token (KM >= k slots held in
+// registers, each chunk's row loads issued before they are added in slot order).
+template <typename E, int KM>
 __global__ void __launch_bounds__(RT_NT)
 combine_kernel(const E* yp, const int32_t* pos, const float* w, E* y, int T, int D, int k) {
   constexpr int VEC = 16 / sizeof(E);
   const int t = blockIdx.x * (RT_NT / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (t >= T) return;
-  int pj[KMAX];
-  float wj[KMAX];
-  for (int j = 0; j < k; ++j) {
-    pj[j] = pos[(int64_t)t * k + j];
-    wj[j] = w[(int64_t)t * k + j];
+  int pj[KM];
+  float wj[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    pj[j] = j < k ? pos[(int64_t)t * k + j] : -1;
+    wj[j] = j < k ? w[(int64_t)t * k + j] : 0.f;
   }
   const int CPR = D / VEC;
   for (int c = lane; c < CPR; c += 64) {
+    uint4 rv[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+      if (pj[j] >= 0) rv[j] = *reinterpret_cast<const uint4*>(yp + (int64_t)pj[j] * D + c * VEC);
     float acc[VEC];
 #pragma unroll
     for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
-    for (int j = 0; j < k; ++j) {
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
       if (pj[j] < 0) continue;
       float v[VEC];
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(yp + (int64_t)pj[j] * D + c * VEC), v);
+      Vec<E>::unpack(rv[j], v);
 #pragma unroll
       for (int i = 0; i < VEC; ++i) acc[i] = fmaf(wj[j], v[i], acc[i]);
     }
@@ -184,8 +191,9 @@ combine_kernel(const E* yp, const int32_t* pos, const float* w, E* y, int T, int
   }
 }
 
-// dy_perm[pos[t,j]] = w[t,j] dy[t];  dw[t,j] = <dy[t], y_perm[pos[t,j]]>
-template <typename E>
+// dy_perm[pos[t,j]] = w[t,j] dy[t];  dw[t,j] = <dy[t], y_perm[pos[t,j]]>  (as combine:
+// KM >= k slots, each chunk's loads issued before use)
+template <typename E, int KM>
 __global__ void __launch_bounds__(RT_NT)
 combine_bwd_kernel(const E* dy, const E* yp, const int32_t* pos, const float* w, E* dyp,
                    float* dw, int T, int D, int k) {
@@ -193,21 +201,28 @@ combine_bwd_kernel(const E* dy, const E* yp, const int32_t* pos, const float* w,
   const int t = blockIdx.x * (RT_NT / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (t >= T) return;
-  int pj[KMAX];
-  float wj[KMAX], dot[KMAX];
-  for (int j = 0; j < k; ++j) {
-    pj[j] = pos[(int64_t)t * k + j];
-    wj[j] = w[(int64_t)t * k + j];
+  int pj[KM];
+  float wj[KM], dot[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    pj[j] = j < k ? pos[(int64_t)t * k + j] : -1;
+    wj[j] = j < k ? w[(int64_t)t * k + j] : 0.f;
     dot[j] = 0.f;
   }
   const int CPR = D / VEC;
   for (int c = lane; c < CPR; c += 64) {
+    const uint4 gv = *reinterpret_cast<const uint4*>(dy + (int64_t)t * D + c * VEC);
+    uint4 rv[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+      if (pj[j] >= 0) rv[j] = *reinterpret_cast<const uint4*>(yp + (int64_t)pj[j] * D + c * VEC);
     float g[VEC];
-    Vec<E>::unpack(*reinterpret_cast<const uint4*>(dy + (int64_t)t * D + c * VEC), g);
-    for (int j = 0; j < k; ++j) {
+    Vec<E>::unpack(gv, g);
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
       if (pj[j] < 0) continue;
       float v[VEC], o[VEC];
-      Vec<E>::unpack(*reinterpret_cast<const uint4*>(yp + (int64_t)pj[j] * D + c * VEC), v);
+      Vec<E>::unpack(rv[j], v);
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < VEC; ++i) {
@@ -218,7 +233,9 @@ combine_bwd_kernel(const E* dy, const E* yp, const int32_t* pos, const float* w,
       *reinterpret_cast<uint4*>(dyp + (int64_t)pj[j] * D + c * VEC) = Vec<E>::pack(o);
     }
   }
-  for (int j = 0; j < k; ++j) {
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    if (j >= k) break;
     const float s = wave_sum(dot[j]);
     if (lane == 0) dw[(int64_t)t * k + j] = pj[j] >= 0 ? s : 0.f;
   }
@@ -385,12 +402,23 @@ extern "C" int dmoe_combine(const dmoe_dims* dims, const void* y_perm, const int
   if (!aligned16(y_perm) || !aligned16(y)) return DMOE_EUNSUPPORTED;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((unsigned)((s.T + 3) / 4));
-  if (s.dtype == DMOE_BF16)
-    DMOE_LAUNCH(combine_kernel<bf16>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(y_perm),
-                       pos, w, reinterpret_cast<bf16*>(y), (int)s.T, (int)s.D, s.k);
-  else
-    DMOE_LAUNCH(combine_kernel<float>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const float*>(y_perm),
-                       pos, w, reinterpret_cast<float*>(y), (int)s.T, (int)s.D, s.k);
+  auto go = [&](auto EK, auto KMc) {
+    using E = typename decltype(EK)::type;
+    constexpr int KM = decltype(KMc)::value;
+    const char* kname = std::is_same<E, bf16>::value ? "combine_kernel<bf16>" : "combine_kernel<float>";
+    DMOE_LAUNCH_NAMED(kname,
+                      (combine_kernel<E, KM>), grid, dim3(RT_NT), 0, st, reinterpret_cast<const E*>(y_perm), pos,
+                      w, reinterpret_cast<E*>(y), (int)s.T, (int)s.D, s.k);
+  };
+  using K4 = std::integral_constant<int, 4>;
+  using K8 = std::integral_constant<int, KMAX>;
+  if (s.dtype == DMOE_BF16) {
+    if (s.k <= 4) go(type_tag<bf16>{}, K4{});
+    else go(type_tag<bf16>{}, K8{});
+  } else {
+    if (s.k <= 4) go(type_tag<float>{}, K4{});
+    else go(type_tag<float>{}, K8{});
+  }
   return launch_status();
 }
 
@@ -405,14 +433,24 @@ extern "C" int dmoe_combine_bwd(const dmoe_dims* dims, const void* dy, const voi
   if (!aligned16(dy) || !aligned16(y_perm) || !aligned16(dy_perm)) return DMOE_EUNSUPPORTED;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid((unsigned)((s.T + 3) / 4));
-  if (s.dtype == DMOE_BF16)
-    DMOE_LAUNCH(combine_bwd_kernel<bf16>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const bf16*>(dy),
-                       reinterpret_cast<const bf16*>(y_perm), pos, w, reinterpret_cast<bf16*>(dy_perm), dw,
-                       (int)s.T, (int)s.D, s.k);
-  else
-    DMOE_LAUNCH(combine_bwd_kernel<float>, grid, dim3(RT_NT), 0, st, reinterpret_cast<const float*>(dy),
-                       reinterpret_cast<const float*>(y_perm), pos, w, reinterpret_cast<float*>(dy_perm), dw,
-                       (int)s.T, (int)s.D, s.k);
+  auto go = [&](auto EK, auto KMc) {
+    using E = typename decltype(EK)::type;
+    constexpr int KM = decltype(KMc)::value;
+    const char* kname = std::is_same<E, bf16>::value ? "combine_bwd_kernel<bf16>" : "combine_bwd_kernel<float>";
+    DMOE_LAUNCH_NAMED(kname,
+                      (combine_bwd_kernel<E, KM>), grid, dim3(RT_NT), 0, st, reinterpret_cast<const E*>(dy),
+                      reinterpret_cast<const E*>(y_perm), pos, w, reinterpret_cast<E*>(dy_perm), dw, (int)s.T,
+                      (int)s.D, s.k);
+  };
+  using K4 = std::integral_constant<int, 4>;
+  using K8 = std::integral_constant<int, KMAX>;
+  if (s.dtype == DMOE_BF16) {
+    if (s.k <= 4) go(type_tag<bf16>{}, K4{});
+    else go(type_tag<bf16>{}, K8{});
+  } else {
+    if (s.k <= 4) go(type_tag<float>{}, K4{});
+    else go(type_tag<float>{}, K8{});
+  }
   return launch_status();
 }
 
@@ -431,7 +469,9 @@ extern "C" int dmoe_dispatch_bwd(const dmoe_dims* dims, const void* dx_perm, con
   auto go = [&](auto EK, auto KMc) {
     using E = typename decltype(EK)::type;
     constexpr int KM = decltype(KMc)::value;
-    DMOE_LAUNCH((dispatch_bwd_kernel<E, KM, 8>), grid, dim3(RT_NT), 0, st,
+    const char* kname = std::is_same<E, bf16>::value ? "dispatch_bwd_kernel<bf16>" : "dispatch_bwd_kernel<float>";
+    DMOE_LAUNCH_NAMED(kname,
+                      (dispatch_bwd_kernel<E, KM, 8>), grid, dim3(RT_NT), 0, st,
                 reinterpret_cast<const E*>(dx_perm), pos, gate ? idx : nullptr, gate ? dg : nullptr,
                 reinterpret_cast<const E*>(Wg), reinterpret_cast<E*>(dx), (int)s.T, (int)s.D, s.k, s.d, s.M);
   };
