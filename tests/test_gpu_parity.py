@@ -54,6 +54,13 @@ CASES = {
     # one group more), token count off the 32-token blocks
     "bf16_wide_gate": Workload("bf16_wide_gate", 19, T=150, D=2112, H=64, d=2, M=16, k=4, dtype="bf16",
                                act="gelu", p_alive=0.9),
+    # degenerate grids of one expert (M = 1): every token's TopK is that expert with
+    # weight 1; one gate column (bf16, MFMA gate, 700 rows on the fat tiles) or two
+    # (fp32, d = 2)
+    "bf16_one_expert": Workload("bf16_one_expert", 32, T=700, D=128, H=128, d=1, M=1, k=1, dtype="bf16",
+                                act="gelu"),
+    "f32_one_expert_2d": Workload("f32_one_expert_2d", 33, T=50, D=64, H=64, d=2, M=1, k=1, dtype="f32",
+                                  act="relu"),
 }
 
 
