@@ -135,6 +135,15 @@ dispatch_scatter(const int32_t* idx, const uint8_t* alive, int P, int N, int k,
   }
 }
 
+// 16-byte store with the non-temporal hint, for large outputs written once in whole
+// 128-byte lines (a wave store covers 1 KB of one row): such lines are not left in the
+// caches as dirty lines that a later kernel's reads must first write back.  (Partial
+// lines written this way lose the caches' write combining.)
+__device__ __forceinline__ void store_stream16(void* p, const uint4& v) {
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
+}
+
 // x_perm[pos[t,j]] = x[t]: each token's row is read once and written to each of its
 // alive pairs' rows (reading per token, not per row, keeps x traffic at one pass).
 template <typename E>
@@ -149,7 +158,7 @@ gather_rows(const E* x, const int32_t* pos, int T, int k, int D, E* xp) {
     const uint4 v = *reinterpret_cast<const uint4*>(x + t * D + c * VEC);
     for (int j = 0; j < k; ++j) {
       const int r = pos[t * k + j];
-      if (r >= 0) *reinterpret_cast<uint4*>(xp + (int64_t)r * D + c * VEC) = v;
+      if (r >= 0) store_stream16(xp + (int64_t)r * D + c * VEC, v);
     }
   }
 }
@@ -241,14 +250,6 @@ combine_bwd_kernel(const E* dy, const E* yp, const int32_t* pos, const float* w,
   }
 }
 
-// 16-byte store with the non-temporal hint, for large outputs written once in whole
-// 128-byte lines (a wave store covers 1 KB of one row): such lines are not left in the
-// caches as dirty lines that a later kernel's reads must first write back.  (Partial
-// lines written this way lose the caches' write combining.)
-__device__ __forceinline__ void store_stream16(void* p, const uint4& v) {
-  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-  __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
-}
 
 // dx[t] = sum_j dx_perm[pos[t,j]]  (+ sum_j dg[t,j] sum_i Wg[i*M + u_i(idx[t,j])]), one
 // wave per token.  The gate share is taken over the token's distinct gate columns c,
