@@ -137,7 +137,9 @@ dispatch_scatter(const int32_t* idx, const uint8_t* alive, int P, int N, int k,
 
 // 16-byte store with the non-temporal hint, for large outputs written once in whole
 // 128-byte lines (a wave store covers 1 KB of one row): such lines are not left in the
-// caches as dirty lines that a later kernel's reads must first write back.  (Partial
+// caches as dirty lines that a later kernel's reads must first write back.  Used for
+// x_perm, y and dx; dy_perm keeps ordinary stores (the dh GEMM right after it reads it
+// faster from the caches: non-temporal measured 5% slower there).  (Partial
 // lines written this way lose the caches' write combining.)
 __device__ __forceinline__ void store_stream16(void* p, const uint4& v) {
   typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -196,7 +198,7 @@ combine_kernel(const E* yp, const int32_t* pos, const float* w, E* y, int T, int
 #pragma unroll
       for (int i = 0; i < VEC; ++i) acc[i] = fmaf(wj[j], v[i], acc[i]);
     }
-    *reinterpret_cast<uint4*>(y + (int64_t)t * D + c * VEC) = Vec<E>::pack(acc);
+    store_stream16(y + (int64_t)t * D + c * VEC, Vec<E>::pack(acc));
   }
 }
 
