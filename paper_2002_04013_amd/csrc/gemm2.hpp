@@ -38,12 +38,14 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 //     those loads; in-order retirement makes them cover the ring loads issued before.
 // The pipeline's counted vmcnt waits and barriers order these loads.
 // The LDS destination is lds_base + LOFF, LOFF a compile-time byte offset, so one
-// scalar register serves every load of a stage.
+// scalar register serves every load of a stage.  The scalar add writes SCC, declared
+// clobbered: the compiler may otherwise hold a compare result, or the carry of a 64-bit
+// address add split around the statement, in SCC across it.
 template <int LOFF>
 __device__ __forceinline__ void g2l_16_at(const bf16* base, uint32_t off_bytes, char* lds_base) {
   const uint32_t m = (uint32_t)(uintptr_t)(lds_ptr_t)lds_base;
   asm volatile("s_add_u32 m0, %2, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :: "v"(off_bytes), "s"(base), "s"(m), "i"(LOFF) : "memory", "m0");
+               :: "v"(off_bytes), "s"(base), "s"(m), "i"(LOFF) : "memory", "m0", "scc");
 }
 
 // f(integral_constant<int, 0>) ... f(integral_constant<int, N-1>), in order
