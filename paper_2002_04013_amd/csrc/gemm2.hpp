@@ -265,6 +265,9 @@ __device__ __forceinline__ int stg_off(int r, int c) { return r * 128 + ((c ^ ((
 // Extra block (XB = 1, GROUP_M with 256 x 256 tiles of 8 waves): a tile holds up to
 // 288 rows, the 32 beyond the first 256 forming a ninth row block that all 8 waves
 // share, wave (wm, wn) computing its 32 x 32 piece at the wave's own column block wm.
+// The wave holds that block's B fragment already (its column block wm), so the piece
+// costs one more A fragment read per step; the loop is compiled once per wm, which
+// names the fragment at compile time.
 // An expert's rows are then split into ceil(rows / 288) tiles of equal block counts, so
 // an expert with a few rows more than a multiple of 256 gets no nearly empty tile
 // (which would stream the expert's whole weight slab again for those rows).
@@ -308,7 +311,7 @@ grouped_gemm2(GemmArgs<bf16> p) {
   // per-lane byte offsets of the MFMA fragments within a stage: K-contiguous tiles by
   // k-step (shared by A and B, whose rows have the same width and swizzle), N-contiguous
   // tiles by 32-column block
-  uint32_t kc_off[KK], a_nc[TM], b_nc[TN], bx_nc = 0;
+  uint32_t kc_off[KK], a_nc[TM], b_nc[TN];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) kc_off[kk] = KcTile<BM, NW, SW, BK>::lane_off(kk * 2, lane);
   if constexpr (A_T) {
@@ -318,7 +321,6 @@ grouped_gemm2(GemmArgs<bf16> p) {
   if constexpr (B_T) {
 #pragma unroll
     for (int i = 0; i < TN; ++i) b_nc[i] = TB::lane_off(wn * TN + i, lane);
-    if constexpr (XB) bx_nc = TB::lane_off(wn * TN + wm, lane);
   }
 
   const int total = ld_plan(p.tprefix, p.groups) * p.tscale;
@@ -482,20 +484,18 @@ grouped_gemm2(GemmArgs<bf16> p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) accx[r] = 0.f;
 
-    auto mainloop = [&](auto NLc, auto XLc) {
+    auto mainloop = [&](auto NLc, auto XLc, auto XCc) {
       constexpr int NL = decltype(NLc)::value;
       constexpr bool XL = decltype(XLc)::value;
-      constexpr int NDS = (A_T ? 2 : 1) * NL + (B_T ? 2 : 1) * TN + (XL ? 1 + (B_T ? 2 : 1) : 0);
-      bf16x8_t fa[2][TM], fb[2][TN], fax[2], fbx[2];
+      constexpr int XC = decltype(XCc)::value;
+      static_assert(!XL || XC < TN, "extra block column within the wave's columns");
+      constexpr int NDS = (A_T ? 2 : 1) * NL + (B_T ? 2 : 1) * TN + (XL ? 1 : 0);
+      bf16x8_t fa[2][TM], fb[2][TN], fax[2];
       auto ldfrag = [&](const char* buf, int kk, int slot) {
         if constexpr (NL == 0) return;             // no rows: nothing to multiply
         const char* as = buf;
         const char* bs = buf + ABYTES;
-        if constexpr (XL) {
-          fax[slot] = TA::frag_at(as, BM, kc_off[kk]);
-          if constexpr (B_T) fbx[slot] = TB::frag_at(bs, kk * 16, bx_nc);
-          else fbx[slot] = TB::frag_at(bs, wn * WTN + wm * 32, kc_off[kk]);
-        }
+        if constexpr (XL) fax[slot] = TA::frag_at(as, BM, kc_off[kk]);
 #pragma unroll
         for (int j = 0; j < NL; ++j) {
           const int r0 = (j * WM + wm) * 32;
@@ -514,7 +514,9 @@ grouped_gemm2(GemmArgs<bf16> p) {
 #pragma unroll
           for (int i = 0; i < TN; ++i)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][i], fa[slot][j], acc[i][j], 0, 0, 0);
-        if constexpr (XL) accx = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fbx[slot], fax[slot], accx, 0, 0, 0);
+        // the extra block's columns are the wave's column block wm (XC, its
+        // compile-time copy): its B fragment is fb[slot][XC]
+        if constexpr (XL) accx = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][XC], fax[slot], accx, 0, 0, 0);
       };
       auto interleave = [&]() {
 #pragma unroll
@@ -586,13 +588,22 @@ grouped_gemm2(GemmArgs<bf16> p) {
       }
     };
     using NoX = std::integral_constant<bool, false>;
-    if (XB && xl) mainloop(std::integral_constant<int, TM>{}, std::integral_constant<bool, (XB != 0)>{});
-    else if (nl == TM) mainloop(std::integral_constant<int, TM>{}, NoX{});
-    else if (TM >= 2 && nl == 1) mainloop(std::integral_constant<int, 1>{}, NoX{});
-    else if (TM >= 3 && nl == 2) mainloop(std::integral_constant<int, (TM >= 3 ? 2 : 1)>{}, NoX{});
-    else if (TM >= 4 && nl == 3) mainloop(std::integral_constant<int, (TM >= 4 ? 3 : 1)>{}, NoX{});
-    else if (TM >= 5 && nl == 4) mainloop(std::integral_constant<int, (TM >= 5 ? 4 : 1)>{}, NoX{});
-    else mainloop(std::integral_constant<int, 0>{}, NoX{});
+    using C0 = std::integral_constant<int, 0>;
+    using XLt = std::integral_constant<bool, (XB != 0)>;
+    using TMt = std::integral_constant<int, TM>;
+    if (XB && xl) {
+      static_assert(!XB || WM == 4, "four wave rows");
+      if (wm == 0) mainloop(TMt{}, XLt{}, C0{});
+      else if (wm == 1) mainloop(TMt{}, XLt{}, std::integral_constant<int, 1>{});
+      else if (wm == 2) mainloop(TMt{}, XLt{}, std::integral_constant<int, (XB ? 2 : 0)>{});
+      else mainloop(TMt{}, XLt{}, std::integral_constant<int, (XB ? 3 : 0)>{});
+    }
+    else if (nl == TM) mainloop(TMt{}, NoX{}, C0{});
+    else if (TM >= 2 && nl == 1) mainloop(std::integral_constant<int, 1>{}, NoX{}, C0{});
+    else if (TM >= 3 && nl == 2) mainloop(std::integral_constant<int, (TM >= 3 ? 2 : 1)>{}, NoX{}, C0{});
+    else if (TM >= 4 && nl == 3) mainloop(std::integral_constant<int, (TM >= 4 ? 3 : 1)>{}, NoX{}, C0{});
+    else if (TM >= 5 && nl == 4) mainloop(std::integral_constant<int, (TM >= 5 ? 4 : 1)>{}, NoX{}, C0{});
+    else mainloop(std::integral_constant<int, 0>{}, NoX{}, C0{});
 
     block_sync_lds();      // every wave is done with the ring before the next tile's loads
 
