@@ -662,12 +662,20 @@ grouped_gemm2(GemmArgs<bf16> p) {
       return n0 + (col < nvalid ? col : 0);
     };
     // the parameter loads are issued for every lane (clamped in range); stores only
-    // where the row and column are valid
+    // where the row and column are valid.  With non-temporal stores the old parameters
+    // are read with the same hint: each is read once, and like the new values it then
+    // streams past the L2 instead of evicting the GEMM's operands.
     uint4 wold[2][4];
     auto load_piece = [&](int pc, uint4 (&dst)[4]) {
+      typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 #pragma unroll
-      for (int qd = 0; qd < 4; ++qd)
-        dst[qd] = *reinterpret_cast<const uint4*>(W + prow(pc, qd) + pcol(pc));
+      for (int qd = 0; qd < 4; ++qd) {
+        const bf16* src = W + prow(pc, qd) + pcol(pc);
+        if constexpr (STO == STORE_STAGED_NT)
+          dst[qd] = __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(src)));
+        else
+          dst[qd] = *reinterpret_cast<const uint4*>(src);
+      }
     };
     if (more) {
       if (early == 0) {
