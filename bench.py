@@ -450,6 +450,30 @@ def run_workload(name, steps, warmup, recompute=False, sgd=False, alive_topk=Fal
     out["call_roofline_untraced"] = {n: roofline_of(alg[n]["flops"], alg[n]["bytes"], ms_u[n] * 1e-3, peak_tf)
                                      for n in timed}
 
+    # The same step recorded once into a HIP graph and replayed: the entry points
+    # allocate nothing and never synchronise, so a caller can run a whole step as one
+    # graph launch.  The replays are timed between two events; the kernels are the same,
+    # only the launch overhead between them changes (what matters for short steps).
+    try:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        n_g = min(steps, 5) if wl.T * wl.D >= (1 << 24) else steps
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(n_g):
+            graph.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        out["graph_ms_per_step"] = g0.elapsed_time(g1) / n_g
+        del graph
+    except RuntimeError as ex:              # reported, not fatal: the eager figures stand
+        out["graph_ms_per_step"] = None
+        out["graph_error"] = str(ex)[:200]
+
     if cold_steps:
         # Cold memory-side cache: before each step, outside any timed interval, write
         # FLUSH_BYTES to one scratch buffer and read FLUSH_BYTES from another, so the
@@ -548,6 +572,10 @@ def summary(r, steps):
            "ms_per_step": round(r["wall"] * 1e3 / steps, 3),
            "tokens_per_s": round(wl.T * steps / r["wall"], 1),
            "step_device_ms_median": round(r["per_step"][len(r["per_step"]) // 2], 4),
+           "graph_replay_ms_per_step": (round(r["graph_ms_per_step"], 4) if r["graph_ms_per_step"] else
+                                        r.get("graph_error")),
+           "graph_replay_tokens_per_s": (round(wl.T / (r["graph_ms_per_step"] * 1e-3), 1)
+                                         if r["graph_ms_per_step"] else None),
            "calls_ms": {n: round(v, 4) for n, v in r["ms"].items()},
            "calls_ms_untraced": {n: round(v, 4) for n, v in r["ms_untraced"].items()},
            "calls_roofline": {n: {k: v[k] for k in ("bound", "achieved", "unit", "frac")}
@@ -650,6 +678,8 @@ def main():
                          "gate_topk and dispatch: 5 more steps with events at call boundaries only"),
         "step_ms": {"median": round(r["per_step"][len(r["per_step"]) // 2], 3), "min": round(r["per_step"][0], 3),
                     "max": round(r["per_step"][-1], 3)},
+        "graph_replay_ms_per_step": (round(r["graph_ms_per_step"], 3) if r["graph_ms_per_step"] else
+                                     r.get("graph_error")),
         "paper_context": PAPER_CONTEXT,
     }
     if "cold" in r:
