@@ -1,0 +1,123 @@
+"""The expert entry points on constructed row counts: every edge of the grouped GEMMs'
+tile schedules.
+
+The expert calls take the row offsets as an input, so the rows per expert are set
+directly here instead of coming out of a routing: empty experts, one row, a row either
+side of the 32-row blocks, of the 256-row tile and of the 288-row tile with its shared
+extra block (257 and 288 rows: one tile whose extra block holds 1 or 32 rows; 289 and
+576/577: two tiles split evenly), experts of 512 +- a few rows like the wide workload's,
+and on the few-rows path a single 301-row expert among many small ones.  D and H are
+multiples of 64 but not of 256, so the last column tile of every GEMM and the last
+tile of every weight gradient are partial.
+
+Forward (h, a, y_perm), backward (dh, dx_perm, dW1, db1, dW2, db2) and the fused SGD
+update are compared element by element with the oracle's expert block (Sec. 3.3, the
+feed-forward experts of Sec. 4.1) in fp64 with the layer's bf16 storage rounding, at
+the bf16 tolerance; gradients of experts without rows must be left untouched."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2002_04013_amd import abi
+from parity_util import RTOL, assert_close, say
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # many rows per expert: 288-row tiles with the extra block, 64-deep weight-gradient steps
+    "fat": dict(d=2, M=4, D=320, H=576, seed=71,
+                counts=[288, 257, 256, 289, 0, 1, 31, 32, 33, 575, 576, 577, 512, 534, 490, 255]),
+    # few rows per expert: 32-row tiles, 32-deep weight-gradient steps over a ring that wraps
+    "skinny": dict(d=2, M=8, D=192, H=320, seed=72,
+                   counts=[0, 1, 2, 3, 31, 32, 33, 63, 64, 65, 301, 7, 0, 16] + [5 + (3 * e) % 29 for e in range(50)]),
+}
+
+
+def _expert_rows(counts, D, H, N, seed, dev):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    P = int(offs[-1]) + 37                               # rows past the last expert stay unused
+    rn = lambda *s, sc=1.0: (torch.randn(*s, generator=g) * sc).to(torch.bfloat16)
+    t = dict(x_perm=rn(P, D), W1=rn(N, H, D, sc=D ** -0.5), b1=rn(N, H, sc=D ** -0.5),
+             W2=rn(N, D, H, sc=H ** -0.5), b2=rn(N, D, sc=H ** -0.5), dy_perm=rn(P, D))
+    return offs, P, t
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_expert_calls_on_tile_edges(name):
+    c = CASES[name]
+    d, M, D, H = c["d"], c["M"], c["D"], c["H"]
+    N = M ** d
+    counts = list(c["counts"]) + [0] * (N - len(c["counts"]))
+    assert len(counts) == N
+    dev = torch.device("cuda:0")
+    offs, P, t = _expert_rows(counts, D, H, N, c["seed"], dev)
+    k = 2
+    T = (P + k - 1) // k
+    Pd = T * k
+    say(f"[expert rows] {name}: N={N} D={D} H={H} rows={int(offs[-1])} P={Pd} counts={counts[:16]}...")
+    pad = lambda v: torch.cat([v, torch.zeros(Pd - P, v.shape[1], dtype=v.dtype)]) if Pd > P else v
+    x_perm, dy_perm = pad(t["x_perm"]).to(dev), pad(t["dy_perm"]).to(dev)
+    W1, b1, W2, b2 = (t[n].to(dev) for n in ("W1", "b1", "W2", "b2"))
+    dims = abi.make_dims(T, D, H, d, M, k, "bf16", "gelu")
+    ws = torch.empty(abi.workspace_bytes(dims), dtype=torch.uint8, device=dev)
+    offsets = torch.from_numpy(offs).to(dev)
+    cnt = torch.tensor(counts, dtype=torch.int32, device=dev)
+    nanb = lambda *s: torch.full(s, float("nan"), dtype=torch.bfloat16, device=dev)
+    h, a, y_perm = nanb(Pd, H), nanb(Pd, H), nanb(Pd, D)
+    abi.dmoe_expert_ffn_fwd(dims, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm, ws)
+    sent = 7.0                                           # experts without rows keep it
+    dh, dx_perm = nanb(Pd, H), nanb(Pd, D)
+    dW1, db1 = torch.full_like(W1, sent), torch.full_like(b1, sent)
+    dW2, db2 = torch.full_like(W2, sent), torch.full_like(b2, sent)
+    abi.dmoe_expert_ffn_bwd(dims, offsets, cnt, x_perm, h, a, dy_perm, W1, W2, dh, dx_perm, dW1, db1, dW2, db2, ws)
+    lr = 0.25
+    sW1, sb1, sW2, sb2 = W1.clone(), b1.clone(), W2.clone(), b2.clone()
+    sdh, sdx = nanb(Pd, H), nanb(Pd, D)
+    abi.dmoe_expert_ffn_bwd_sgd(dims, offsets, cnt, x_perm, h, a, dy_perm, sW1, sb1, sW2, sb2, lr, sdh, sdx, ws)
+    torch.cuda.synchronize()
+    say(f"[expert rows] {name}: GPU calls done")
+
+    cpu = lambda v: v.float().cpu().numpy().astype(np.float64)
+    g = {n: cpu(v) for n, v in dict(h=h, a=a, y=y_perm, dh=dh, dx=dx_perm, dW1=dW1, db1=db1, dW2=dW2, db2=db2,
+                                     sdh=sdh, sdx=sdx, sW1=sW1, sb1=sb1, sW2=sW2, sb2=sb2).items()}
+    X, dY = cpu(x_perm), cpu(dy_perm)
+    P1 = {n: cpu(v) for n, v in dict(W1=W1, b1=b1, W2=W2, b2=b2).items()}
+    rt = RTOL["bf16"]
+    st = O.round_bf16
+    used = int(offs[-1])
+    for n in ("h", "a", "y", "dh", "dx", "sdh", "sdx"):          # rows past the last expert
+        assert np.isnan(g[n][used:]).all(), f"{name}: {n} written past the last expert's rows"
+    for e in range(N):
+        r0, r1 = int(offs[e]), int(offs[e + 1])
+        if r1 == r0:
+            for n in ("dW1", "db1", "dW2", "db2"):
+                assert (g[n][e] == sent).all(), f"{name}: expert {e} without rows: {n} was written"
+            for n, p in (("sW1", "W1"), ("sb1", "b1"), ("sW2", "W2"), ("sb2", "b2")):
+                assert (g[n][e] == P1[p][e]).all(), f"{name}: expert {e} without rows: {p} was updated"
+            continue
+        Xe, dYe = X[r0:r1], dY[r0:r1]
+        hr, ar, yr = O.expert_forward_stored(Xe, P1["W1"][e], P1["b1"][e], P1["W2"][e], P1["b2"][e], "gelu", store=st)
+        dXr, dW1r, db1r, dW2r, db2r = O.expert_backward(Xe, hr, ar, dYe, P1["W1"][e], P1["W2"][e], "gelu", store=st)
+        dHr = st((dYe @ P1["W2"][e]) * O.act_grad(hr, "gelu"))
+        tag = f"{name} expert {e} ({r1 - r0} rows)"
+        assert_close(g["h"][r0:r1], hr, rt, f"{tag}: h")
+        assert_close(g["a"][r0:r1], ar, rt, f"{tag}: a")
+        assert_close(g["y"][r0:r1], yr, rt, f"{tag}: y_perm")
+        assert_close(g["dh"][r0:r1], dHr, rt, f"{tag}: dh")
+        assert_close(g["dx"][r0:r1], dXr, rt, f"{tag}: dx_perm")
+        assert_close(g["dW1"][e], dW1r, rt, f"{tag}: dW1")
+        assert_close(g["db1"][e], db1r, rt, f"{tag}: db1")
+        assert_close(g["dW2"][e], dW2r, rt, f"{tag}: dW2")
+        assert_close(g["db2"][e], db2r, rt, f"{tag}: db2")
+        # the fused update uses the parameters as they were on entry for dh and dx_perm
+        assert torch.equal(sdh[r0:r1], dh[r0:r1]) and torch.equal(sdx[r0:r1], dx_perm[r0:r1]), \
+            f"{tag}: the SGD backward's dh / dx_perm differ from the plain backward's"
+        for n, p, gr in (("sW1", "W1", dW1r), ("sb1", "b1", db1r), ("sW2", "W2", dW2r), ("sb2", "b2", db2r)):
+            ref = O.sgd_step(P1[p][e], gr, lr)
+            # one storage ulp of the update plus lr times the gradient's tolerance
+            lim = 2.0 ** -7 * np.abs(ref) + lr * rt * (np.abs(gr) + np.sqrt(np.mean(gr * gr)))
+            err = np.abs(g[n][e] - ref)
+            assert (err <= lim + 1e-30).all(), f"{tag}: {p} after SGD, worst err {err.max():.3g}"
+    say(f"[expert rows] {name}: every expert matches")
