@@ -13,7 +13,8 @@ tile of every weight gradient are partial.
 Forward (h, a, y_perm), backward (dh, dx_perm, dW1, db1, dW2, db2) and the fused SGD
 update are compared element by element with the oracle's expert block (Sec. 3.3, the
 feed-forward experts of Sec. 4.1) in fp64 with the layer's bf16 storage rounding, at
-the bf16 tolerance; gradients of experts without rows must be left untouched."""
+the bf16 tolerance (an fp32 layer on the fp32 GEMMs at the fp32 one); gradients of
+experts without rows must be left untouched."""
 import numpy as np
 import pytest
 import torch
@@ -31,14 +32,16 @@ CASES = {
     # few rows per expert: 32-row tiles, 32-deep weight-gradient steps over a ring that wraps
     "skinny": dict(d=2, M=8, D=192, H=320, seed=72,
                    counts=[0, 1, 2, 3, 31, 32, 33, 63, 64, 65, 301, 7, 0, 16] + [5 + (3 * e) % 29 for e in range(50)]),
+    # fp32 layer: the register-staged fp32 GEMMs (32 x 64 tiles)
+    "f32": dict(d=2, M=3, D=64, H=128, seed=73, dtype="f32", counts=[0, 1, 31, 32, 33, 63, 64, 65, 97]),
 }
 
 
-def _expert_rows(counts, D, H, N, seed, dev):
+def _expert_rows(counts, D, H, N, seed, dt):
     g = torch.Generator(device="cpu").manual_seed(seed)
     offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
     P = int(offs[-1]) + 37                               # rows past the last expert stay unused
-    rn = lambda *s, sc=1.0: (torch.randn(*s, generator=g) * sc).to(torch.bfloat16)
+    rn = lambda *s, sc=1.0: (torch.randn(*s, generator=g) * sc).to(dt)
     t = dict(x_perm=rn(P, D), W1=rn(N, H, D, sc=D ** -0.5), b1=rn(N, H, sc=D ** -0.5),
              W2=rn(N, D, H, sc=H ** -0.5), b2=rn(N, D, sc=H ** -0.5), dy_perm=rn(P, D))
     return offs, P, t
@@ -52,19 +55,21 @@ def test_expert_calls_on_tile_edges(name):
     counts = list(c["counts"]) + [0] * (N - len(c["counts"]))
     assert len(counts) == N
     dev = torch.device("cuda:0")
-    offs, P, t = _expert_rows(counts, D, H, N, c["seed"], dev)
+    dtype = c.get("dtype", "bf16")
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    offs, P, t = _expert_rows(counts, D, H, N, c["seed"], dt)
     k = 2
     T = (P + k - 1) // k
     Pd = T * k
-    say(f"[expert rows] {name}: N={N} D={D} H={H} rows={int(offs[-1])} P={Pd} counts={counts[:16]}...")
+    say(f"[expert rows] {name}: {dtype} N={N} D={D} H={H} rows={int(offs[-1])} P={Pd} counts={counts[:16]}...")
     pad = lambda v: torch.cat([v, torch.zeros(Pd - P, v.shape[1], dtype=v.dtype)]) if Pd > P else v
     x_perm, dy_perm = pad(t["x_perm"]).to(dev), pad(t["dy_perm"]).to(dev)
     W1, b1, W2, b2 = (t[n].to(dev) for n in ("W1", "b1", "W2", "b2"))
-    dims = abi.make_dims(T, D, H, d, M, k, "bf16", "gelu")
+    dims = abi.make_dims(T, D, H, d, M, k, dtype, "gelu")
     ws = torch.empty(abi.workspace_bytes(dims), dtype=torch.uint8, device=dev)
     offsets = torch.from_numpy(offs).to(dev)
     cnt = torch.tensor(counts, dtype=torch.int32, device=dev)
-    nanb = lambda *s: torch.full(s, float("nan"), dtype=torch.bfloat16, device=dev)
+    nanb = lambda *s: torch.full(s, float("nan"), dtype=dt, device=dev)
     h, a, y_perm = nanb(Pd, H), nanb(Pd, H), nanb(Pd, D)
     abi.dmoe_expert_ffn_fwd(dims, offsets, x_perm, W1, b1, W2, b2, h, a, y_perm, ws)
     sent = 7.0                                           # experts without rows keep it
@@ -84,8 +89,9 @@ def test_expert_calls_on_tile_edges(name):
                                      sdh=sdh, sdx=sdx, sW1=sW1, sb1=sb1, sW2=sW2, sb2=sb2).items()}
     X, dY = cpu(x_perm), cpu(dy_perm)
     P1 = {n: cpu(v) for n, v in dict(W1=W1, b1=b1, W2=W2, b2=b2).items()}
-    rt = RTOL["bf16"]
-    st = O.round_bf16
+    rt = RTOL[dtype]
+    st = O.round_bf16 if dtype == "bf16" else O.round_f32
+    ulp = 2.0 ** -7 if dtype == "bf16" else 2.0 ** -23      # one storage ulp, relative
     used = int(offs[-1])
     for n in ("h", "a", "y", "dh", "dx", "sdh", "sdx"):          # rows past the last expert
         assert np.isnan(g[n][used:]).all(), f"{name}: {n} written past the last expert's rows"
@@ -117,7 +123,7 @@ def test_expert_calls_on_tile_edges(name):
         for n, p, gr in (("sW1", "W1", dW1r), ("sb1", "b1", db1r), ("sW2", "W2", dW2r), ("sb2", "b2", db2r)):
             ref = O.sgd_step(P1[p][e], gr, lr)
             # one storage ulp of the update plus lr times the gradient's tolerance
-            lim = 2.0 ** -7 * np.abs(ref) + lr * rt * (np.abs(gr) + np.sqrt(np.mean(gr * gr)))
+            lim = ulp * np.abs(ref) + lr * rt * (np.abs(gr) + np.sqrt(np.mean(gr * gr)))
             err = np.abs(g[n][e] - ref)
             assert (err <= lim + 1e-30).all(), f"{tag}: {p} after SGD, worst err {err.max():.3g}"
     say(f"[expert rows] {name}: every expert matches")
