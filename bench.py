@@ -102,17 +102,18 @@ _GEMM2 = re.compile(r"grouped_gemm2<GM=(\d),AT=(\d),BT=(\d),EPI=(\d)")
 
 
 def kernel_algorithmic(name, wl, counts, sgd=False):
-    """(role, flops, bytes) of one launch of kernel `name` in a Linear-act-Linear layer,
-    or None for kernels without a per-launch closed form here.  A grouped GEMM launch
-    multiplies every alive pair's row once (2 rows D H flops) and reads each touched
-    expert's weight matrix once; the per-row operands and outputs are read or written
-    once."""
-    if wl.expert != "ffn":
-        return None
+    """(role, flops, bytes) of one launch of kernel `name`, or None for kernels without a
+    per-launch closed form here.  A grouped GEMM launch multiplies every alive pair's row
+    once (2 rows n_in n_out flops) and reads each touched expert's weight matrix once;
+    the per-row operands and outputs are read or written once.  The LayerNorm block
+    launches each GEMM kind once per linear layer (D->F, F->F, F->D): its figures are
+    the mean over the three, matching the mean launch time they are divided by."""
     e = 2 if wl.dtype == "bf16" else 4
     T, D, H, k, dM = wl.T, wl.D, wl.H, wl.k, wl.dM
     rows = int(sum(counts))
     touched = int(sum(1 for c in counts if c > 0))
+    if wl.expert == "ffblock":
+        return _block_kernel_algorithmic(name, wl, rows, touched, e)
     w = touched * D * H * e
     f = 2 * rows * D * H
     m = _GEMM2.match(name)
@@ -129,6 +130,11 @@ def kernel_algorithmic(name, wl, counts, sgd=False):
         if epi == 0 and bt == 1:   # dx_perm = dh W1: read dh, W1; write dx_perm
             return "expert dx GEMM", f, w + rows * (H + D) * e
         return None
+    return _routing_kernel_algorithmic(name, wl, rows, e)
+
+
+def _routing_kernel_algorithmic(name, wl, rows, e):
+    T, D, k, dM = wl.T, wl.D, wl.k, wl.dM
     if name.startswith("gate_topk_mfma"):
         return "gate scores + TopK (MFMA)", 2 * T * D * dM, T * D * e + dM * D * e + T * k * 12
     if name.startswith("gather_rows"):
@@ -140,6 +146,37 @@ def kernel_algorithmic(name, wl, counts, sgd=False):
     if name.startswith("dispatch_bwd_kernel"):
         return "dispatch backward", 0, rows * D * e + T * D * e + T * k * 8
     return None
+
+
+def _block_kernel_algorithmic(name, wl, rows, touched, e):
+    """Per-launch figures of the LayerNorm block layer's kernels (Linear D->F, LayerNorm +
+    act, Linear F->F, LayerNorm + act, Linear F->D): GEMMs as the mean over the three
+    linear layers; the LayerNorm row kernels read and write each [rows, F] tensor once,
+    plus 8 bytes of fp32 statistics per row and the touched experts' scale and shift."""
+    D, F = wl.D, wl.H
+    layers = ((D, F), (F, F), (F, D))
+    m = _GEMM2.match(name)
+    if m:
+        gm, bt, epi = int(m.group(1)), int(m.group(3)), int(m.group(4))
+        fl = sum(2 * rows * a * b for a, b in layers) // 3
+        wts = sum(touched * a * b * e for a, b in layers) // 3
+        if gm == 1:       # weight gradients: both row operands in, every touched dW out
+            return ("block weight-gradient GEMM (mean of 3 layers)", fl,
+                    sum(rows * (a + b) * e for a, b in layers) // 3 + wts)
+        if epi == 1:      # forward with bias: rows in, weights and bias in, rows out
+            return ("block forward GEMM (mean of 3 layers)", fl,
+                    wts + sum(touched * b * e + rows * (a + b) * e for a, b in layers) // 3)
+        if epi == 0 and bt == 1:   # data gradients
+            return "block data-gradient GEMM (mean of 3 layers)", fl, wts + sum(rows * (a + b) * e for a, b in layers) // 3
+        return None
+    lnp = 2 * touched * F * e + 8 * rows
+    if name.startswith("(ln_act_fwd_kernel"):
+        return "LayerNorm + act forward", 0, 2 * rows * F * e + lnp
+    if name.startswith("(ln_act_bwd_rows_kernel"):
+        return "LayerNorm + act backward (rows)", 0, 3 * rows * F * e + lnp
+    if name.startswith("(ln_act_bwd_params_kernel"):
+        return "LayerNorm + act backward (scale, shift)", 0, 2 * rows * F * e + lnp + 2 * touched * F * e
+    return _routing_kernel_algorithmic(name, wl, rows, e)
 
 
 def roofline_of(flops, nbytes, seconds, peak_tf):

@@ -69,3 +69,26 @@ def test_kernel_rooflines_closed_forms():
     assert fl == a["ffn_fwd"]["flops"] + a["ffn_bwd"]["flops"]
     r = bench.roofline_of(dw[1], dw[2], 0.02, bench.PEAK_BF16_TFLOPS)
     assert r["bound"] == "mfma" and abs(r["achieved"] - dw[1] / 0.02 / 1e12) < 0.1
+
+
+def test_block_kernel_rooflines_closed_forms():
+    """The LayerNorm block layer's per-launch figures: each GEMM kind is launched once per
+    linear layer, so three launches of the three kinds add up to the call totals, and the
+    LayerNorm row kernels move each [rows, F] tensor once."""
+    import bench
+    from workloads import get_workload
+    wl = get_workload("ffblock")
+    counts = [wl.T * wl.k // wl.N] * wl.N
+    P, D, F, e = wl.T * wl.k, wl.D, wl.H, 2
+    b = bench.algorithmic_block(wl, counts)
+    fwd = bench.kernel_algorithmic("grouped_gemm2<GM=0,AT=0,BT=0,EPI=1,288x256,ST=2,BK=64,XB>", wl, counts)
+    dgr = bench.kernel_algorithmic("grouped_gemm2<GM=0,AT=0,BT=1,EPI=0,288x256,ST=2,BK=64,XB>", wl, counts)
+    wgr = bench.kernel_algorithmic("grouped_gemm2<GM=1,AT=1,BT=1,EPI=0,256x256,ST=2,BK=64>", wl, counts)
+    assert 3 * fwd[1] == b["ffn_fwd"]["flops"]
+    assert 3 * (dgr[1] + wgr[1]) == b["ffn_bwd"]["flops"]
+    # weight gradients: both row operands once, every expert's gradient written once
+    assert 3 * wgr[2] == P * (2 * D + 2 * F + 2 * F) * e + wl.N * (2 * D * F + F * F) * e
+    ln = bench.kernel_algorithmic("(ln_act_fwd_kernel<E, 8, ACT>)", wl, counts)
+    assert ln[1] == 0 and ln[2] == 2 * P * F * e + 8 * P + 2 * wl.N * F * e
+    r = bench.roofline_of(ln[1], ln[2], 1e-3, bench.PEAK_BF16_TFLOPS)
+    assert r["bound"] == "hbm"
