@@ -251,7 +251,9 @@ __device__ __forceinline__ int stg_off(int r, int c) { return r * 128 + ((c ^ ((
 //     while the MFMAs of step kk run, and in the last step the wave waits for stage
 //     kt+1, passes the barrier, refills the ring slot of stage kt with stage
 //     kt+STAGES and reads the first fragments of stage kt+1, all before issuing the
-//     last MFMAs of stage kt, so no LDS latency is exposed at stage boundaries;
+//     last MFMAs of stage kt, so no LDS latency is exposed at stage boundaries (the
+//     row-grouped GEMMs with N-contiguous weights issue those MFMAs before the wait
+//     instead, see MM_EARLY);
 //   * vector-memory operations (loads, stores, direct-to-LDS loads) retire from the
 //     vmcnt counter in issue order on gfx9-family chips, so "stage s has landed" is
 //     vmcnt <= (operations issued after stage s).  The previous tile's epilogue stores
