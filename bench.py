@@ -660,7 +660,7 @@ def main():
         return
     ws_env = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or ws_env != 1:
-        print("bench.py: this build runs the DMoE layer on one GPU only; "
+        print("bench.py: the DMoE layer path here runs on one GPU only; "
               "multi-GPU (--gpus > 1) is not supported", file=sys.stderr)
         sys.exit(2)
 
