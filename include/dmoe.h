@@ -40,7 +40,10 @@
  *     called from several host threads.  (2) The launch trace below, per host thread.
  *     (3) The 131328-byte device array of dmoe_expert_ffn_fwd_noalloc, per device.
  *   - Supported: 1 <= d <= 4, 1 <= M, d*M <= 128, 1 <= k <= min(N, 8),
- *     N <= 16384, T >= 0, D and H multiples of 64 and at most 2^22, pointers 16-byte aligned.
+ *     N <= 16384, T >= 0 and T*k < 2^30, D and H multiples of 64 and at most 2^22,
+ *     pointers 16-byte aligned.  Dims outside these give DMOE_EINVAL where they make no
+ *     sense (T < 0, D or H or d or M or k < 1, k > N, unknown dtype, act or flag bits)
+ *     and DMOE_EUNSUPPORTED where they are only beyond the supported set.
  *
  * Return codes: DMOE_OK (0); DMOE_EINVAL (-1) null required pointer or bad
  * dims; DMOE_EUNSUPPORTED (-2) shape/alignment outside the supported set;

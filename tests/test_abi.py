@@ -133,3 +133,38 @@ def test_gate_workspace_required_on_host(lib):
         dims = lib.make_dims(64, 64, 256, 2, 4, 2, dt, "relu", flags)
         rc = raw.dmoe_gate_topk(ctypes.byref(dims), F(), F(), None, None, F(), F(), None, None, None, None)
         assert rc == -1, (dt, flags)
+
+
+@pytest.mark.parametrize("case,kw,rc", [
+    ("T < 0", dict(T=-1), -1),
+    ("D = 0", dict(D=0), -1),
+    ("H = 0", dict(H=0), -1),
+    ("d = 0", dict(d=0), -1),
+    ("M = 0", dict(M=0), -1),
+    ("k = 0", dict(k=0), -1),
+    ("k > N", dict(d=1, M=2, k=3), -1),
+    ("unknown dtype", dict(dtype=7), -1),
+    ("unknown activation", dict(act=9), -1),
+    ("unknown flag bit", dict(flags=0x80), -1),
+    ("d > 4", dict(d=5, M=2), -2),
+    ("N > 16384", dict(d=2, M=129), -2),
+    ("k > 8", dict(d=2, M=4, k=9), -2),
+    ("d M > 128", dict(d=2, M=65), -2),
+    ("D not a multiple of 64", dict(D=96), -2),
+    ("H not a multiple of 64", dict(H=200), -2),
+    ("D above 2^22", dict(D=(1 << 22) + 64), -2),
+    ("T k at 2^30", dict(T=1 << 28, k=4), -2),
+])
+def test_dims_rules_on_host(lib, case, kw, rc):
+    """The supported-set rules of the header: each invalid dims is refused by the entry
+    point before any device work (the pointers below are never dereferenced), and the
+    workspace query answers 0 for it."""
+    raw = lib.load()
+    base = dict(T=64, D=64, H=256, d=2, M=4, k=2, dtype=lib.DMOE_BF16, act=lib.DMOE_RELU, flags=0)
+    base.update(kw)
+    dims = lib.Dims(*(int(base[f]) for f in ("T", "D", "H", "d", "M", "k", "dtype", "act", "flags")))
+    got = raw.dmoe_gate_topk(ctypes.byref(dims), *[_fake() for _ in range(9)], None)
+    assert got == rc, f"{case}: dmoe_gate_topk returned {got}, expected {rc}"
+    assert lib.workspace_bytes(dims) == 0, case
+    ok = lib.make_dims(64, 64, 256, 2, 4, 2, "bf16", "relu")
+    assert lib.workspace_bytes(ok) > 0
